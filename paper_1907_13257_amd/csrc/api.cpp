@@ -1,0 +1,361 @@
+// api.cpp -- the C ABI of liblstm355: argument validation, buffer layout
+// of `reserve` and `workspace`, and the order of kernel launches for one
+// layer's forward pass and back-propagation through time.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "../../include/lstm355.h"
+#include "kernels.hpp"
+
+using namespace lstm355;
+
+struct lstm_handle {
+    lstm_desc_t d;
+    DType dt;
+    size_t es;
+    int Hr;
+    long ldx, ldy;
+    long TB, G4;
+    // reserve layout (bytes)
+    size_t r_gates, r_cs, r_ms, r_total;
+    // workspace layout (bytes)
+    size_t w_sync, w_dz, w_rt, w_pt, w_dH, w_dcn, w_dhn, w_part, w_total;
+    // per-device tiling
+    int dev;
+    int num_cus;
+    bool fwd_ok, bwd_ok;
+    RecTiling fwd, bwd;
+};
+
+namespace {
+
+thread_local char g_detail[256] = "";
+
+void set_detail(const char *what, hipError_t e)
+{
+    std::snprintf(g_detail, sizeof(g_detail), "%s: %s", what, hipGetErrorString(e));
+}
+
+lstm_status_t hip_status(const char *what, hipError_t e)
+{
+    if (e == hipSuccess) return LSTM_OK;
+    set_detail(what, e);
+    if (e == hipErrorCooperativeLaunchTooLarge) return LSTM_ERR_UNSUPPORTED;
+    return LSTM_ERR_HIP;
+}
+
+lstm_status_t invalid(const char *what)
+{
+    std::snprintf(g_detail, sizeof(g_detail), "invalid argument: %s", what);
+    return LSTM_ERR_INVALID_ARG;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+lstm_status_t ensure_plan(lstm_handle *h)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status("hipGetDevice", e);
+    if (h->dev == dev) return LSTM_OK;
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_status("hipDeviceGetAttribute", e);
+    RecShape sh{h->d.T, h->d.B, h->d.I, h->d.H, h->d.Hp, h->d.reverse, h->ldy};
+    h->fwd_ok = plan_forward(h->dt, sh, cus, &h->fwd);
+    h->bwd_ok = plan_backward(h->dt, sh, cus, &h->bwd);
+    h->num_cus = cus;
+    h->dev = dev;
+    return LSTM_OK;
+}
+
+#define TRY_HIP(what, expr)                                  \
+    do {                                                     \
+        hipError_t e_ = (expr);                              \
+        if (e_ != hipSuccess) return hip_status(what, e_);   \
+    } while (0)
+
+}  // namespace
+
+extern "C" const char *lstm_last_error_detail(void) { return g_detail; }
+
+extern "C" const char *lstm_status_string(lstm_status_t s)
+{
+    switch (s) {
+    case LSTM_OK: return "LSTM_OK";
+    case LSTM_ERR_INVALID_ARG: return "LSTM_ERR_INVALID_ARG";
+    case LSTM_ERR_UNSUPPORTED: return "LSTM_ERR_UNSUPPORTED";
+    case LSTM_ERR_WORKSPACE: return "LSTM_ERR_WORKSPACE";
+    case LSTM_ERR_HIP: return "LSTM_ERR_HIP";
+    case LSTM_ERR_TIMEOUT: return "LSTM_ERR_TIMEOUT";
+    }
+    return "LSTM_ERR_UNKNOWN";
+}
+
+extern "C" lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out)
+{
+    try {
+        if (!desc || !out) return invalid("desc/out is NULL");
+        *out = nullptr;
+        const lstm_desc_t &d = *desc;
+        if (d.T < 1 || d.B < 1 || d.I < 1 || d.H < 1) return invalid("T, B, I, H must be positive");
+        if (d.Hp < 0) return invalid("Hp must be >= 0");
+        if (d.dtype != LSTM_F32 && d.dtype != LSTM_BF16) return invalid("unknown dtype");
+        if (d.reverse != 0 && d.reverse != 1) return invalid("reverse must be 0 or 1");
+        if (d.I % 8 || d.H % 8 || d.Hp % 8) return invalid("I, H and Hp must be multiples of 8");
+        const int Hr = d.Hp ? d.Hp : d.H;
+        const long ldx = d.ldx ? d.ldx : d.I;
+        const long ldy = d.ldy ? d.ldy : Hr;
+        if (ldx < d.I || ldx % 8) return invalid("ldx must be >= I and a multiple of 8");
+        if (ldy < Hr || ldy % 8) return invalid("ldy must be >= the output width and a multiple of 8");
+        const long TB = (long)d.T * d.B;
+        const long G4 = 4L * d.H;
+        if (TB > (1L << 31) / 1 || G4 * (long)(ldx > G4 ? ldx : G4) > (1L << 40) || TB * G4 > (1L << 40))
+            return invalid("sizes too large");
+
+        lstm_handle *h = new (std::nothrow) lstm_handle();
+        if (!h) return invalid("out of host memory");
+        h->d = d;
+        h->dt = d.dtype == LSTM_BF16 ? DType::BF16 : DType::F32;
+        h->es = dsize(h->dt);
+        h->Hr = Hr;
+        h->ldx = ldx;
+        h->ldy = ldy;
+        h->TB = TB;
+        h->G4 = G4;
+        size_t o = 0;
+        h->r_gates = o; o = align256(o + (size_t)TB * G4 * 4);
+        h->r_cs = o;    o = align256(o + (size_t)TB * d.H * 4);
+        h->r_ms = o;    o = align256(o + (d.Hp ? (size_t)TB * d.H * h->es : 0));
+        h->r_total = o;
+        o = 0;
+        h->w_sync = o; o = align256(o + SYNC_BYTES);
+        h->w_dz = o;   o = align256(o + (size_t)TB * G4 * h->es);
+        h->w_rt = o;   o = align256(o + (size_t)Hr * G4 * h->es);
+        h->w_pt = o;   o = align256(o + (d.Hp ? (size_t)d.H * d.Hp * h->es : 0));
+        h->w_dH = o;   o = align256(o + (d.Hp ? (size_t)TB * d.Hp * h->es : 0));
+        h->w_dcn = o;  o = align256(o + (size_t)d.B * d.H * 4);
+        h->w_dhn = o;  o = align256(o + (size_t)d.B * d.H * 4);
+        h->w_part = o; o = align256(o + colsum_partial_floats((int)TB, (int)G4) * 4);
+        h->w_total = o;
+        h->dev = -1;
+        h->fwd_ok = h->bwd_ok = false;
+        *out = h;
+        return LSTM_OK;
+    } catch (...) {
+        return invalid("exception");
+    }
+}
+
+extern "C" size_t lstm_reserve_size(lstm_handle_t h) { return h ? h->r_total : 0; }
+extern "C" size_t lstm_workspace_size(lstm_handle_t h) { return h ? h->w_total : 0; }
+
+extern "C" lstm_status_t lstm_destroy(lstm_handle_t h)
+{
+    delete h;
+    return LSTM_OK;
+}
+
+extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
+                                      const void *R, const float *b, const void *P, void *y, void *hT, float *cT,
+                                      void *reserve, void *workspace, void *stream)
+{
+    try {
+        if (!h) return invalid("handle is NULL");
+        const lstm_desc_t &d = h->d;
+        if (!x || !W || !R || !b || !y || !reserve || !workspace) return invalid("required pointer is NULL");
+        if ((P != nullptr) != (d.Hp > 0)) return invalid("P must be given iff Hp > 0");
+        for (const void *p : {x, h0, W, R, P, (const void *)y, (const void *)hT, (const void *)reserve, (const void *)workspace})
+            if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+        for (const void *p : {(const void *)c0, (const void *)b, (const void *)cT})
+            if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+        lstm_status_t st = ensure_plan(h);
+        if (st != LSTM_OK) return st;
+        if (!h->fwd_ok) {
+            std::snprintf(g_detail, sizeof(g_detail), "no forward tiling fits this device");
+            return LSTM_ERR_UNSUPPORTED;
+        }
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        char *rv = static_cast<char *>(reserve);
+        char *wv = static_cast<char *>(workspace);
+        float *gates = reinterpret_cast<float *>(rv + h->r_gates);
+
+        GemmDesc g{};
+        g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
+        g.M = (int)h->TB; g.N = (int)h->G4; g.K = d.I;
+        g.A = x; g.lda = h->ldx;
+        g.B = W; g.ldb = d.I;
+        g.C = gates; g.ldc = h->G4;
+        g.bias = b; g.beta = 0;
+        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+
+        RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, h->ldy};
+        FwdBufs fb{};
+        fb.R = R; fb.P = P; fb.h0 = h0; fb.c0 = c0;
+        fb.gates = gates;
+        fb.cs = reinterpret_cast<float *>(rv + h->r_cs);
+        fb.ms = d.Hp ? rv + h->r_ms : nullptr;
+        fb.y = y; fb.hT = hT; fb.cT = cT;
+        fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
+        TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
+        return LSTM_OK;
+    } catch (...) {
+        return invalid("exception");
+    }
+}
+
+extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const void *dhT, const float *dcT,
+                                       const void *x, const void *h0, const float *c0, const void *W, const void *R,
+                                       const void *P, const void *y, const void *reserve, void *dx, void *dh0,
+                                       float *dc0, float *dW, float *dR, float *db, float *dP, int accumulate,
+                                       void *workspace, void *stream)
+{
+    try {
+        if (!h) return invalid("handle is NULL");
+        const lstm_desc_t &d = h->d;
+        if (!dy || !x || !W || !R || !y || !reserve || !workspace || !dW || !dR || !db)
+            return invalid("required pointer is NULL");
+        if ((P != nullptr) != (d.Hp > 0)) return invalid("P must be given iff Hp > 0");
+        if (d.Hp > 0 && !dP) return invalid("dP is required for LSTMP");
+        if (accumulate != 0 && accumulate != 1) return invalid("accumulate must be 0 or 1");
+        for (const void *p : {dy, dhT, x, h0, W, R, P, y, reserve, (const void *)dx, (const void *)dh0, (const void *)workspace})
+            if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+        for (const void *p : {(const void *)dcT, (const void *)c0, (const void *)dc0, (const void *)dW,
+                              (const void *)dR, (const void *)db, (const void *)dP})
+            if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+        lstm_status_t st = ensure_plan(h);
+        if (st != LSTM_OK) return st;
+        if (!h->bwd_ok) {
+            std::snprintf(g_detail, sizeof(g_detail), "no backward tiling fits this device");
+            return LSTM_ERR_UNSUPPORTED;
+        }
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        const char *rv = static_cast<const char *>(reserve);
+        char *wv = static_cast<char *>(workspace);
+        const int T = d.T, B = d.B, I = d.I, H = d.H, Hp = d.Hp, Hr = h->Hr;
+        const long G4 = h->G4, TB = h->TB;
+        const size_t es = h->es;
+        void *dz = wv + h->w_dz;
+        void *Rt = wv + h->w_rt;
+        void *Pt = Hp ? wv + h->w_pt : nullptr;
+        void *dH = Hp ? wv + h->w_dH : nullptr;
+
+        TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s));
+        if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
+
+        RecShape sh{T, B, I, H, Hp, d.reverse, h->ldy};
+        BwdBufs bb{};
+        bb.Rt = Rt; bb.Pt = Pt; bb.dy = dy; bb.dhT = dhT; bb.dcT = dcT; bb.h0 = h0; bb.c0 = c0;
+        bb.gates = reinterpret_cast<const float *>(rv + h->r_gates);
+        bb.cs = reinterpret_cast<const float *>(rv + h->r_cs);
+        bb.dz = dz; bb.dH = dH;
+        bb.dcn = reinterpret_cast<float *>(wv + h->w_dcn);
+        bb.dhn = reinterpret_cast<float *>(wv + h->w_dhn);
+        bb.dh0 = dh0; bb.dc0 = dc0;
+        bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
+        TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
+
+        if (dx) {  // dX = dZ W
+            GemmDesc g{};
+            g.in = h->dt; g.out_f32 = h->dt == DType::F32; g.a_kmajor = true; g.b_kmajor = false;
+            g.M = (int)TB; g.N = I; g.K = (int)G4;
+            g.A = dz; g.lda = G4; g.B = W; g.ldb = I; g.C = dx; g.ldc = h->ldx;
+            TRY_HIP("dx", gemm(g, s, K_GEMM_DX));
+        }
+        {  // dW = dZ^T X
+            GemmDesc g{};
+            g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+            g.M = (int)G4; g.N = I; g.K = (int)TB;
+            g.A = dz; g.lda = G4; g.B = x; g.ldb = h->ldx; g.C = dW; g.ldc = I; g.beta = accumulate;
+            TRY_HIP("dW", gemm(g, s, K_GEMM_DW));
+        }
+        {  // dR = sum_t dz_t^T h_{t-1}: steps after the first see y of the previous step, the first sees h0
+            int beta = accumulate;
+            const char *dzc = static_cast<const char *>(dz);
+            const char *yc = static_cast<const char *>(y);
+            if (T > 1) {
+                GemmDesc g{};
+                g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+                g.M = (int)G4; g.N = Hr; g.K = (T - 1) * B;
+                if (!d.reverse) {
+                    g.A = dzc + (size_t)B * G4 * es;   // dz at t = 1 .. T-1
+                    g.B = yc;                          // y  at t = 0 .. T-2
+                } else {
+                    g.A = dzc;                                  // dz at t = 0 .. T-2
+                    g.B = yc + (size_t)B * h->ldy * es;         // y  at t = 1 .. T-1
+                }
+                g.lda = G4; g.ldb = h->ldy; g.C = dR; g.ldc = Hr; g.beta = beta;
+                TRY_HIP("dR", gemm(g, s, K_GEMM_DR));
+                beta = 1;
+            }
+            if (h0) {
+                const int tf = d.reverse ? T - 1 : 0;
+                GemmDesc g{};
+                g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+                g.M = (int)G4; g.N = Hr; g.K = B;
+                g.A = dzc + (size_t)tf * B * G4 * es; g.lda = G4;
+                g.B = h0; g.ldb = Hr; g.C = dR; g.ldc = Hr; g.beta = beta;
+                TRY_HIP("dR(h0)", gemm(g, s, K_GEMM_DR));
+                beta = 1;
+            }
+            if (!beta) TRY_HIP("dR zero", fill_u32(dR, (size_t)G4 * Hr, 0u, s));
+        }
+        TRY_HIP("db", colsum(h->dt, dz, (int)TB, (int)G4, reinterpret_cast<float *>(wv + h->w_part), db, accumulate, s));
+        if (Hp) {  // dP = sum_t dh_t^T m_t
+            GemmDesc g{};
+            g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+            g.M = Hp; g.N = H; g.K = (int)TB;
+            g.A = dH; g.lda = Hp; g.B = rv + h->r_ms; g.ldb = H; g.C = dP; g.ldc = H; g.beta = accumulate;
+            TRY_HIP("dP", gemm(g, s, K_GEMM_DP));
+        }
+        return LSTM_OK;
+    } catch (...) {
+        return invalid("exception");
+    }
+}
+
+extern "C" lstm_status_t lstm_check(lstm_handle_t h, void *workspace, void *stream)
+{
+    if (!h || !workspace) return invalid("handle/workspace is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    TRY_HIP("stream sync", hipStreamSynchronize(s));
+    unsigned tripped = 0;
+    TRY_HIP("read watchdog flag", watchdog_read_and_clear(&tripped));
+    if (tripped) {
+        std::snprintf(g_detail, sizeof(g_detail), "a grid barrier's watchdog expired");
+        return LSTM_ERR_TIMEOUT;
+    }
+    return LSTM_OK;
+}
+
+extern "C" lstm_status_t lstm_add(lstm_dtype_t dtype, size_t n, const void *a, const void *b, void *out, void *stream)
+{
+    if (dtype != LSTM_F32 && dtype != LSTM_BF16) return invalid("unknown dtype");
+    if (n == 0) return LSTM_OK;
+    if (!a || !b || !out) return invalid("NULL pointer");
+    TRY_HIP("add", add(dtype == LSTM_BF16 ? DType::BF16 : DType::F32, n, a, b, out, static_cast<hipStream_t>(stream)));
+    return LSTM_OK;
+}
+
+/* Tiling chosen for this handle on the current device (diagnostics). */
+extern "C" lstm_status_t lstm_describe_tiling(lstm_handle_t h, int *out8)
+{
+    if (!h || !out8) return invalid("NULL pointer");
+    lstm_status_t st = ensure_plan(h);
+    if (st != LSTM_OK) return st;
+    out8[0] = h->fwd_ok ? h->fwd.G : 0;
+    out8[1] = h->fwd.HN;
+    out8[2] = h->fwd.BM;
+    out8[3] = h->fwd.variant;
+    out8[4] = h->bwd_ok ? h->bwd.G : 0;
+    out8[5] = h->bwd.HN;
+    out8[6] = h->bwd.BM;
+    out8[7] = h->bwd.variant;
+    return LSTM_OK;
+}

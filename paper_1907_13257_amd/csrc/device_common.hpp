@@ -1,0 +1,87 @@
+// device_common.hpp -- storage types, conversions, gate non-linearities and
+// matrix-core (MFMA) wrappers shared by the gfx950 kernels of liblstm355.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lstm355 {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// Storage types: bf16 values travel as their 16-bit patterns.
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float(((unsigned)v) << 16); }
+
+// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f)
+{
+    unsigned u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u)
+        return (bf16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+template <typename TI> __device__ __forceinline__ TI from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// Gate non-linearities in fp32.  sigma(u) = 1/(1+e^-u); tanh(u) = 2 sigma(2u) - 1.
+// Both saturate correctly: e^-u overflows to +inf for very negative u, giving 0.
+__device__ __forceinline__ float sigmoid_f(float u) { return 1.0f / (1.0f + __expf(-u)); }
+__device__ __forceinline__ float tanh_f(float u) { return 2.0f / (1.0f + __expf(-2.0f * u)) - 1.0f; }
+
+// ---------------------------------------------------------------------------
+// MFMA wrappers.  A "fragment" is the 16 bytes one lane contributes per
+// operand: 8 bf16 or 4 fp32 values consecutive along k.
+//
+// 16x16 output block (C[16][16], 4 fp32 per lane: row 4*(lane/16)+v, col lane%16).
+//   Operand row (A: output row, B: output col) = lane % 16, and lane group
+//   q = lane / 16 (0..3) supplies k = q*E .. q*E+E-1 of a 4E-wide k chunk
+//   (E = elements per fragment).  bf16: one v_mfma_f32_16x16x32_bf16 covers
+//   the 32-wide chunk.  fp32: four v_mfma_f32_16x16x4f32, element e of every
+//   lane group in the e-th instruction.  The sum over k does not depend on
+//   which lane holds which k, so A and B only have to agree, which they do
+//   by construction.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void mfma16(f32x4 &acc, u32x4 a, u32x4 b, bf16_t)
+{
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                  acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mfma16(f32x4 &acc, u32x4 a, u32x4 b, float)
+{
+    f32x4 fa = __builtin_bit_cast(f32x4, a), fb = __builtin_bit_cast(f32x4, b);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[0], fb[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[1], fb[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[2], fb[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[3], fb[3], acc, 0, 0, 0);
+}
+
+// 32x32 output block (16 fp32 per lane: row 8*(v/4) + 4*(lane/32) + v%4,
+// col lane%32).  Operand row = lane % 32; lane group q = lane / 32 (0..1)
+// supplies k = q*E .. q*E+E-1 of a 2E-wide chunk.
+__device__ __forceinline__ void mfma32(f32x16 &acc, u32x4 a, u32x4 b, bf16_t)
+{
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                  acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mfma32(f32x16 &acc, u32x4 a, u32x4 b, float)
+{
+    f32x4 fa = __builtin_bit_cast(f32x4, a), fb = __builtin_bit_cast(f32x4, b);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[0], fb[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[1], fb[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[2], fb[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[3], fb[3], acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ u32x4 ldg16(const void *p) { return *reinterpret_cast<const u32x4 *>(p); }
+__device__ __forceinline__ u32x4 zero16() { return u32x4{0u, 0u, 0u, 0u}; }
+
+}  // namespace lstm355

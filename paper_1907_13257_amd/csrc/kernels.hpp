@@ -1,0 +1,125 @@
+// kernels.hpp -- host-side launch interface of the liblstm355 kernels
+// (declarations shared by api.cpp and the .hip translation units).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lstm355 {
+
+enum class DType { F32 = 0, BF16 = 1 };
+
+inline size_t dsize(DType t) { return t == DType::BF16 ? 2 : 4; }
+
+// Kernel classes for the timing hooks (profile.cpp).
+enum KClass {
+    K_GEMM_GX = 0,   // input projection X W^T + b
+    K_REC_FWD,       // persistent forward recurrence
+    K_REC_BWD,       // persistent BPTT recurrence
+    K_GEMM_DX,       // dX = dZ W
+    K_GEMM_DW,       // dW = dZ^T X
+    K_GEMM_DR,       // dR = dZ^T H_prev
+    K_GEMM_DP,       // dP = dH^T M
+    K_SMALL,         // transposes, column sums, fills, adds
+    K_NCLASS
+};
+const char *kclass_name(int k);
+
+// Timing hooks: bracket one launch with events when profiling is on.
+struct ProfScope {
+    ProfScope(int kclass, hipStream_t s, double flops, double bytes);
+    ~ProfScope();
+    int k;
+    hipStream_t s;
+    double flops, bytes;
+    void *ev0;
+};
+
+// C[m][n] (beta ? C : 0) + sum_k A(m,k) B(n,k) (+ bias[n])
+//   A(m,k) = a_kmajor ? A[m*lda + k] : A[k*lda + m]
+//   B(n,k) = b_kmajor ? B[n*ldb + k] : B[k*ldb + n]
+// Inputs share one element type; C is fp32 or the input type.
+struct GemmDesc {
+    DType in;
+    bool out_f32;
+    bool a_kmajor, b_kmajor;
+    int M, N, K;
+    const void *A; long lda;
+    const void *B; long ldb;
+    void *C; long ldc;
+    const float *bias;
+    int beta;
+};
+hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
+
+// Small kernels.
+hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s);  // dst[c][r] = src[r][c]
+hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
+// dst[c] (+)= sum_r src[r][c] over a [rows][cols] matrix of element type t, in fp32, deterministic;
+// `partial` holds colsum_partial_floats(rows, cols) floats of scratch.
+size_t colsum_partial_floats(int rows, int cols);
+hipError_t colsum(DType t, const void *src, int rows, int cols, float *partial, float *dst, int accumulate, hipStream_t s);
+hipError_t add(DType t, size_t n, const void *a, const void *b, void *out, hipStream_t s);
+
+// Persistent recurrence kernels (recurrent.hip).
+struct RecShape {
+    int T, B, I, H, Hp, reverse;
+    long ldy;
+};
+struct RecTiling {
+    int HN;      // cells per workgroup
+    int BM;      // batch rows per tile
+    int nHT;     // hidden tiles
+    int nBT;     // batch tiles
+    int G;       // workgroups (cooperative grid)
+    int bgroups; // workgroups per hidden tile
+    int variant; // kernel instantiation index
+    size_t lds;  // dynamic LDS bytes
+};
+// Chooses a tiling for the forward / backward kernels; false if none fits.
+bool plan_forward(DType t, const RecShape &sh, int num_cus, RecTiling *out);
+bool plan_backward(DType t, const RecShape &sh, int num_cus, RecTiling *out);
+
+struct FwdBufs {
+    const void *R, *P, *h0;
+    const float *c0;
+    float *gates;   // [T][B][4H]: in Gx (with bias), out activated gates
+    float *cs;      // [T][B][H]
+    void *ms;       // [T][B][H] (LSTMP)
+    void *y;
+    void *hT;
+    float *cT;
+    unsigned *sync;
+};
+hipError_t launch_forward(DType t, const RecShape &sh, const RecTiling &tl, const FwdBufs &b, hipStream_t s);
+
+struct BwdBufs {
+    const void *Rt;     // R^T [Hr][4H]
+    const void *Pt;     // P^T [H][Hp] (LSTMP)
+    const void *dy;     // [T][B][Ho] stride ldy
+    const void *dhT;
+    const float *dcT;
+    const void *h0;
+    const float *c0;
+    const float *gates, *cs;
+    void *dz;           // [T][B][4H]
+    void *dH;           // [T][B][Hp] (LSTMP)
+    float *dcn;         // [B][H] carry of dc between steps
+    float *dhn;         // [B][H] carry of dh between steps (plain LSTM)
+    void *dh0;
+    float *dc0;
+    unsigned *sync;
+};
+hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, const BwdBufs &b, hipStream_t s);
+
+// Workspace layout of the sync block (bytes); zeroed before every launch.
+constexpr size_t SYNC_BYTES = 1024;
+constexpr int SYNC_COUNT0 = 0;     // u32 index of barrier counter
+constexpr int SYNC_ABORT = 64;     // u32 index of this launch's abort flag
+constexpr int SYNC_WORDS = 128;    // u32 words cleared before each launch
+
+// Reads (synchronously) and clears the library's sticky watchdog word on the
+// current device: nonzero if a grid barrier gave up since the last call.
+hipError_t watchdog_read_and_clear(unsigned *tripped);
+
+}  // namespace lstm355

@@ -1,0 +1,706 @@
+// recurrent.hip -- the sequential part of the LSTM step: one persistent,
+// cooperatively launched kernel for the forward recurrence and one for
+// back-propagation through time.  Each visits all T steps with a grid-wide
+// barrier between dependent steps.
+//
+// Ownership.  Workgroup (ht, bg) owns the cells j in [ht*HN, ht*HN + HN) for
+// the batch tiles bt = bg, bg + bgroups, ...  Forward: the workgroup keeps the
+// 4*HN rows of R that feed its cells (all four gates of each cell, so the gate
+// math stays local) in LDS for the whole kernel and, per step, multiplies
+// h_{t-1} of its batch rows by them on the matrix cores, adds the
+// precomputed input projection and applies the cell update.  Backward: it
+// keeps the HN columns of R (rows of R^T) for its cells and computes, per
+// step, the gate gradients of its cells and then their share of
+// dh_{t-1} = R^T dz.
+//
+// Barrier.  Every thread fences its stores at agent scope, the workgroup
+// meets at s_barrier, then one lane increments a counter in the workspace
+// and spins until all workgroups have arrived.  The counter is monotonic
+// within a launch (target = k * gridDim.x at the k-th barrier) and zeroed by
+// a fill kernel before each launch.  The spin has a wall-clock watchdog: on
+// expiry it raises an abort flag (so every other workgroup leaves too) and a
+// sticky error word of the library (a device variable, zero at load) that the
+// host reads and clears with lstm_check.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+#include <algorithm>
+
+namespace lstm355 {
+
+namespace {
+
+constexpr int WGT = 256;
+
+}  // namespace
+
+__device__ unsigned g_watchdog_tripped = 0;
+
+namespace {
+
+__device__ __forceinline__ bool grid_barrier(unsigned *sync, unsigned target, unsigned long long timeout)
+{
+    __shared__ int s_abort;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int ab = 0;
+        __hip_atomic_fetch_add(sync + SYNC_COUNT0, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long t0 = wall_clock64();
+        while (__hip_atomic_load(sync + SYNC_COUNT0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (__hip_atomic_load(sync + SYNC_ABORT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                ab = 1;
+                break;
+            }
+            if (wall_clock64() - t0 > timeout) {
+                __hip_atomic_store(&g_watchdog_tripped, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(sync + SYNC_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ab = 1;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        s_abort = ab;
+    }
+    __syncthreads();
+    return s_abort == 0;
+}
+
+// Distributed product out[m][n] = sum_k A[m][k] * Bt[n][k] over the whole
+// grid: 16x16 output blocks are dealt to workgroups, K is split over the four
+// waves and the partials are summed through LDS (`red`, 4 KiB).  Used for the
+// projection h_t = P m_t and for the LSTMP carry R^T dz, whose reductions
+// span every workgroup's cells.
+template <typename TI, typename Epi>
+__device__ __forceinline__ void dist_product(const char *A, long lda, const char *Bt, long ldb, int M, int N, int K,
+                                             float *red, Epi epi)
+{
+    constexpr int E = 16 / (int)sizeof(TI), KC = 4 * E;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nbm = (M + 15) / 16, nbn = (N + 15) / 16;
+    const int nkc = (K + KC - 1) / KC;
+    for (int blk = blockIdx.x; blk < nbm * nbn; blk += gridDim.x) {
+        const int mb = blk / nbn, nb = blk % nbn;
+        const int m = mb * 16 + (lane & 15), n = nb * 16 + (lane & 15);
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int kc = wave; kc < nkc; kc += 4) {
+            const int k = kc * KC + (lane >> 4) * E;
+            const u32x4 fa = (m < M && k < K) ? ldg16(A + ((long)m * lda + k) * (long)sizeof(TI)) : zero16();
+            const u32x4 fb = (n < N && k < K) ? ldg16(Bt + ((long)n * ldb + k) * (long)sizeof(TI)) : zero16();
+            mfma16(acc, fa, fb, TI{});
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[wave * 256 + (4 * (lane >> 4) + v) * 16 + (lane & 15)] = acc[v];
+        __syncthreads();
+        {
+            const int r = tid >> 4, c = tid & 15;
+            const int mm = mb * 16 + r, nn = nb * 16 + c;
+            const float v = red[r * 16 + c] + red[256 + r * 16 + c] + red[512 + r * 16 + c] + red[768 + r * 16 + c];
+            if (mm < M && nn < N) epi(mm, nn, v);
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// forward
+// ---------------------------------------------------------------------------
+struct FwdArgs {
+    int T, B, H, Hp, Hr, reverse;
+    long ldy;
+    const char *R, *P, *h0;
+    const float *c0;
+    float *gates, *cs;
+    char *ms, *y, *hT;
+    float *cT;
+    unsigned *sync;
+    unsigned long long timeout;
+    int HN, nHT, nBT, bgroups, r_lds, kpitch;
+};
+
+// Waves: kq = wave & 1 takes every other k chunk, nq = wave >> 1 takes half of
+// the 4*HN gate rows (NBW blocks of 16).  MB blocks of 16 batch rows.
+template <typename TI, int MB, int NBW>
+__global__ __launch_bounds__(WGT) void lstm_fwd_kernel(FwdArgs a)
+{
+    constexpr int E = 16 / (int)sizeof(TI), KC = 4 * E;
+    constexpr int BM = 16 * MB, NT = 32 * NBW;
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    float *zbuf = reinterpret_cast<float *>(lds);           // [2][BM][NT]
+    char *rs = lds + 2 * BM * NT * 4;                        // [NT][kpitch]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kq = wave & 1, nq = wave >> 1;
+    const int HN = a.HN;                                     // == NT / 4
+    const int ht = blockIdx.x % a.nHT, bg = blockIdx.x / a.nHT;
+    const int j0 = ht * HN;
+    const int H = a.H, Hr = a.Hr, B = a.B;
+    const int nkc = (Hr + KC - 1) / KC;
+    const long G4 = 4L * H;
+
+    if (a.r_lds) {
+        const int vpr = nkc * 4;                             // 16-byte vectors per row
+        for (int idx = tid; idx < NT * vpr; idx += WGT) {
+            const int n = idx / vpr, kv = idx % vpr;
+            const int g = n / HN, j = j0 + n % HN, k = kv * E;
+            u32x4 v = zero16();
+            if (j < H && k < Hr) v = ldg16(a.R + ((long)(g * H + j) * Hr + k) * (long)sizeof(TI));
+            *reinterpret_cast<u32x4 *>(rs + n * a.kpitch + kv * 16) = v;
+        }
+    }
+    __syncthreads();
+
+    unsigned nbar = 0;
+    int tprev = -1;
+    for (int s = 0; s < a.T; ++s) {
+        const int t = a.reverse ? a.T - 1 - s : s;
+        const char *hprev = s == 0 ? a.h0 : a.y + (long)tprev * B * a.ldy * (long)sizeof(TI);
+        const long ldh = s == 0 ? Hr : a.ldy;
+        const bool last = s == a.T - 1;
+
+        for (int bt = bg; bt < a.nBT; bt += a.bgroups) {
+            const int b0 = bt * BM;
+            f32x4 acc[MB][NBW];
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int jn = 0; jn < NBW; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+            if (hprev) {
+                for (int kc = kq; kc < nkc; kc += 2) {
+                    const int k = kc * KC + (lane >> 4) * E;
+                    u32x4 fa[MB], fb[NBW];
+#pragma unroll
+                    for (int i = 0; i < MB; ++i) {
+                        const int b = b0 + i * 16 + (lane & 15);
+                        fa[i] = (b < B && k < Hr) ? ldg16(hprev + ((long)b * ldh + k) * (long)sizeof(TI)) : zero16();
+                    }
+#pragma unroll
+                    for (int jn = 0; jn < NBW; ++jn) {
+                        const int n = (nq * NBW + jn) * 16 + (lane & 15);
+                        if (a.r_lds) {
+                            fb[jn] = *reinterpret_cast<const u32x4 *>(rs + n * a.kpitch + k * (int)sizeof(TI));
+                        } else {
+                            const int g = n / HN, j = j0 + n % HN;
+                            fb[jn] = (j < H && k < Hr) ? ldg16(a.R + ((long)(g * H + j) * Hr + k) * (long)sizeof(TI))
+                                                       : zero16();
+                        }
+                    }
+#pragma unroll
+                    for (int i = 0; i < MB; ++i)
+#pragma unroll
+                        for (int jn = 0; jn < NBW; ++jn) mfma16(acc[i][jn], fa[i], fb[jn], TI{});
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int jn = 0; jn < NBW; ++jn)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int row = i * 16 + 4 * (lane >> 4) + v;
+                        const int col = (nq * NBW + jn) * 16 + (lane & 15);
+                        zbuf[(kq * BM + row) * NT + col] = acc[i][jn][v];
+                    }
+            __syncthreads();
+
+            for (int e = tid; e < BM * HN; e += WGT) {
+                const int bl = e / HN, u = e % HN;
+                const int b = b0 + bl, j = j0 + u;
+                if (b >= B || j >= H) continue;
+                float *gx = a.gates + ((long)t * B + b) * G4;
+                const float *z0 = zbuf + bl * NT, *z1 = zbuf + (BM + bl) * NT;
+                const float zi = z0[u] + z1[u] + gx[j];
+                const float zf = z0[HN + u] + z1[HN + u] + gx[H + j];
+                const float zg = z0[2 * HN + u] + z1[2 * HN + u] + gx[2 * H + j];
+                const float zo = z0[3 * HN + u] + z1[3 * HN + u] + gx[3 * H + j];
+                const float ig = sigmoid_f(zi), fg = sigmoid_f(zf), gg = tanh_f(zg), og = sigmoid_f(zo);
+                const float cp = s == 0 ? (a.c0 ? a.c0[(long)b * H + j] : 0.0f) : a.cs[((long)tprev * B + b) * H + j];
+                const float c = fg * cp + ig * gg;
+                const float m = og * tanh_f(c);
+                gx[j] = ig;
+                gx[H + j] = fg;
+                gx[2 * H + j] = gg;
+                gx[3 * H + j] = og;
+                a.cs[((long)t * B + b) * H + j] = c;
+                const TI mv = from_f32<TI>(m);
+                if (a.Hp) {
+                    reinterpret_cast<TI *>(a.ms)[((long)t * B + b) * H + j] = mv;
+                } else {
+                    reinterpret_cast<TI *>(a.y)[((long)t * B + b) * a.ldy + j] = mv;
+                    if (last && a.hT) reinterpret_cast<TI *>(a.hT)[(long)b * Hr + j] = mv;
+                }
+                if (last && a.cT) a.cT[(long)b * H + j] = c;
+            }
+            __syncthreads();
+        }
+
+        if (a.Hp) {
+            // h_t = P m_t needs every cell's m_t
+            if (!grid_barrier(a.sync, ++nbar * gridDim.x, a.timeout)) return;
+            const char *mt = a.ms + (long)t * B * H * (long)sizeof(TI);
+            TI *yt = reinterpret_cast<TI *>(a.y) + (long)t * B * a.ldy;
+            TI *hT = reinterpret_cast<TI *>(a.hT);
+            const long ldy = a.ldy;
+            dist_product<TI>(mt, H, a.P, H, B, a.Hp, H, zbuf, [&](int b, int p, float v) {
+                const TI hv = from_f32<TI>(v);
+                yt[(long)b * ldy + p] = hv;
+                if (last && hT) hT[(long)b * Hr + p] = hv;
+            });
+        }
+        if (!last && !grid_barrier(a.sync, ++nbar * gridDim.x, a.timeout)) return;
+        tprev = t;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// backward
+// ---------------------------------------------------------------------------
+struct BwdArgs {
+    int T, B, H, Hp, Hr, reverse;
+    long ldy;
+    const char *Rt, *Pt, *dy, *dhT;
+    const float *dcT, *c0, *gates, *cs;
+    char *dz, *dH, *dh0;
+    float *dc0;
+    float *dcn, *dhn;       // per-cell carries [B][H]
+    unsigned *sync;
+    unsigned long long timeout;
+    int HN, nHT, nBT, bgroups, w_lds, kpitch;
+};
+
+// Product over K of a tile's rows of A (global) with the workgroup's weight
+// slice (LDS or global) into red[4][BM][NT]; all four waves split K.
+template <typename TI, int MB, int NBW>
+__device__ __forceinline__ void tile_product(const char *A, long lda, int b0, int B, int K, const char *ws, int kpitch,
+                                             const char *wg_rows, long wg_ld, int nrows, float *red)
+{
+    constexpr int E = 16 / (int)sizeof(TI), KC = 4 * E;
+    constexpr int BM = 16 * MB, NT = 16 * NBW;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nkc = (K + KC - 1) / KC;
+    f32x4 acc[MB][NBW];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int jn = 0; jn < NBW; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kc = wave; kc < nkc; kc += 4) {
+        const int k = kc * KC + (lane >> 4) * E;
+        u32x4 fa[MB], fb[NBW];
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const int b = b0 + i * 16 + (lane & 15);
+            fa[i] = (b < B && k < K) ? ldg16(A + ((long)b * lda + k) * (long)sizeof(TI)) : zero16();
+        }
+#pragma unroll
+        for (int jn = 0; jn < NBW; ++jn) {
+            const int n = jn * 16 + (lane & 15);
+            if (ws) {
+                fb[jn] = *reinterpret_cast<const u32x4 *>(ws + n * kpitch + k * (int)sizeof(TI));
+            } else {
+                fb[jn] = (n < nrows && k < K) ? ldg16(wg_rows + ((long)n * wg_ld + k) * (long)sizeof(TI)) : zero16();
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int jn = 0; jn < NBW; ++jn) mfma16(acc[i][jn], fa[i], fb[jn], TI{});
+    }
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int jn = 0; jn < NBW; ++jn)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                red[(wave * BM + i * 16 + 4 * (lane >> 4) + v) * NT + jn * 16 + (lane & 15)] = acc[i][jn][v];
+}
+
+template <typename TI, int MB, int NBW, bool PROJ>
+__global__ __launch_bounds__(WGT) void lstm_bwd_kernel(BwdArgs a)
+{
+    constexpr int BM = 16 * MB, NT = 16 * NBW;
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    float *red = reinterpret_cast<float *>(lds);             // [4][BM][NT] (>= 4 KiB)
+    constexpr int RED_BYTES = (4 * BM * NT * 4 > 4096) ? 4 * BM * NT * 4 : 4096;
+    char *ws = lds + RED_BYTES;                              // [NT][kpitch]
+
+    const int tid = threadIdx.x;
+    const int HN = a.HN;
+    const int ht = blockIdx.x % a.nHT, bg = blockIdx.x / a.nHT;
+    const int j0 = ht * HN;
+    const int H = a.H, Hr = a.Hr, B = a.B, Hp = a.Hp;
+    const long G4 = 4L * H;
+    const int Kw = PROJ ? Hp : 4 * H;                        // k extent of the LDS slice
+    const char *wsrc = PROJ ? a.Pt : a.Rt;                   // rows j of P^T or R^T
+
+    if (a.w_lds) {
+        constexpr int E = 16 / (int)sizeof(TI);
+        const int vpr = (Kw + 4 * E - 1) / (4 * E) * 4;
+        for (int idx = tid; idx < NT * vpr; idx += WGT) {
+            const int n = idx / vpr, kv = idx % vpr;
+            const int j = j0 + n, k = kv * E;
+            u32x4 v = zero16();
+            if (n < HN && j < H && k < Kw) v = ldg16(wsrc + ((long)j * Kw + k) * (long)sizeof(TI));
+            *reinterpret_cast<u32x4 *>(ws + n * a.kpitch + kv * 16) = v;
+        }
+    }
+    const char *wsl = a.w_lds ? ws : nullptr;
+    const char *wrows = wsrc + (long)j0 * Kw * (long)sizeof(TI);
+    const int nrows = min(HN, H - j0);
+    unsigned nbar = 0;
+
+    if (PROJ) {
+        // dh of the first visited step (in reverse order): dy + dhT
+        const int t = a.reverse ? 0 : a.T - 1;
+        TI *dHt = reinterpret_cast<TI *>(a.dH) + (long)t * B * Hp;
+        const TI *dyt = reinterpret_cast<const TI *>(a.dy) + (long)t * B * a.ldy;
+        const TI *dhT = reinterpret_cast<const TI *>(a.dhT);
+        for (long i = (long)blockIdx.x * WGT + tid; i < (long)B * Hp; i += (long)gridDim.x * WGT) {
+            const long b = i / Hp, p = i % Hp;
+            float v = to_f32(dyt[b * a.ldy + p]);
+            if (dhT) v += to_f32(dhT[b * Hp + p]);
+            dHt[i] = from_f32<TI>(v);
+        }
+        if (!grid_barrier(a.sync, ++nbar * gridDim.x, a.timeout)) return;
+    } else {
+        __syncthreads();
+    }
+
+    for (int s = a.T - 1; s >= 0; --s) {
+        const int t = a.reverse ? a.T - 1 - s : s;
+        const int tp = a.reverse ? t + 1 : t - 1;            // previously visited step in the forward order
+        const bool first = s == a.T - 1;
+
+        for (int bt = bg; bt < a.nBT; bt += a.bgroups) {
+            const int b0 = bt * BM;
+            if (PROJ) {
+                // dm = P^T dh for this tile's rows and the workgroup's cells
+                const char *dHt = a.dH + (long)t * B * Hp * (long)sizeof(TI);
+                tile_product<TI, MB, NBW>(dHt, Hp, b0, B, Hp, wsl, a.kpitch, wrows, Kw, nrows, red);
+                __syncthreads();
+            }
+            for (int e = tid; e < BM * HN; e += WGT) {
+                const int bl = e / HN, u = e % HN;
+                const int b = b0 + bl, j = j0 + u;
+                if (b >= B || j >= H) continue;
+                const long cell = (long)b * H + j;
+                float dm;
+                if (PROJ) {
+                    dm = red[(0 * BM + bl) * NT + u] + red[(1 * BM + bl) * NT + u] + red[(2 * BM + bl) * NT + u] +
+                         red[(3 * BM + bl) * NT + u];
+                } else {
+                    dm = to_f32(reinterpret_cast<const TI *>(a.dy)[((long)t * B + b) * a.ldy + j]);
+                    if (first) {
+                        if (a.dhT) dm += to_f32(reinterpret_cast<const TI *>(a.dhT)[(long)b * Hr + j]);
+                    } else {
+                        dm += a.dhn[cell];
+                    }
+                }
+                const float *g4 = a.gates + ((long)t * B + b) * G4;
+                const float ig = g4[j], fg = g4[H + j], gg = g4[2 * H + j], og = g4[3 * H + j];
+                const float c = a.cs[((long)t * B + b) * H + j];
+                const float cp = s == 0 ? (a.c0 ? a.c0[cell] : 0.0f) : a.cs[((long)tp * B + b) * H + j];
+                const float dcin = first ? (a.dcT ? a.dcT[cell] : 0.0f) : a.dcn[cell];
+                const float tc = tanh_f(c);
+                const float d_o = dm * tc;
+                const float d_c = dcin + dm * og * (1.0f - tc * tc);
+                const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cp;
+                TI *dz = reinterpret_cast<TI *>(a.dz) + ((long)t * B + b) * G4;
+                dz[j] = from_f32<TI>(d_i * ig * (1.0f - ig));
+                dz[H + j] = from_f32<TI>(d_f * fg * (1.0f - fg));
+                dz[2 * H + j] = from_f32<TI>(d_g * (1.0f - gg * gg));
+                dz[3 * H + j] = from_f32<TI>(d_o * og * (1.0f - og));
+                const float dcn = d_c * fg;
+                a.dcn[cell] = dcn;
+                if (s == 0 && a.dc0) a.dc0[cell] = dcn;
+            }
+            __syncthreads();
+        }
+
+        // dh_{t-1} = R^T dz_t needs every cell's dz_t
+        if (!grid_barrier(a.sync, ++nbar * gridDim.x, a.timeout)) return;
+        const char *dzt = a.dz + (long)t * B * G4 * (long)sizeof(TI);
+        if (PROJ) {
+            TI *dh0 = reinterpret_cast<TI *>(a.dh0);
+            if (s > 0 || dh0) {
+                TI *dHp = s > 0 ? reinterpret_cast<TI *>(a.dH) + (long)tp * B * Hp : nullptr;
+                const TI *dyp = s > 0 ? reinterpret_cast<const TI *>(a.dy) + (long)tp * B * a.ldy : nullptr;
+                const long ldy = a.ldy;
+                dist_product<TI>(dzt, G4, a.Rt, G4, B, Hp, (int)G4, red, [&](int b, int p, float v) {
+                    if (dHp) {
+                        dHp[(long)b * Hp + p] = from_f32<TI>(v + to_f32(dyp[(long)b * ldy + p]));
+                    } else {
+                        dh0[(long)b * Hp + p] = from_f32<TI>(v);
+                    }
+                });
+            }
+            if (s > 0 && !grid_barrier(a.sync, ++nbar * gridDim.x, a.timeout)) return;
+        } else {
+            if (s == 0 && !a.dh0) break;
+            for (int bt = bg; bt < a.nBT; bt += a.bgroups) {
+                const int b0 = bt * BM;
+                tile_product<TI, MB, NBW>(dzt, G4, b0, B, (int)G4, wsl, a.kpitch, wrows, Kw, nrows, red);
+                __syncthreads();
+                for (int e = tid; e < BM * HN; e += WGT) {
+                    const int bl = e / HN, u = e % HN;
+                    const int b = b0 + bl, j = j0 + u;
+                    if (b >= B || j >= H) continue;
+                    const float v = red[(0 * BM + bl) * NT + u] + red[(1 * BM + bl) * NT + u] +
+                                    red[(2 * BM + bl) * NT + u] + red[(3 * BM + bl) * NT + u];
+                    if (s > 0)
+                        a.dhn[(long)b * H + j] = v;
+                    else
+                        reinterpret_cast<TI *>(a.dh0)[(long)b * Hr + j] = from_f32<TI>(v);
+                }
+                __syncthreads();
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host side: tiling choice and launch
+// ---------------------------------------------------------------------------
+int g_lds_limit = 0;
+unsigned long long g_timeout_ticks = 0;
+
+void device_limits()
+{
+    if (g_lds_limit) return;
+    int dev = 0, lds = 0, khz = 0;
+    (void)hipGetDevice(&dev);
+    if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || lds <= 0)
+        lds = 64 * 1024;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) khz = 100000;
+    g_lds_limit = lds;
+    g_timeout_ticks = (unsigned long long)khz * 1000ull * 2ull;  // 2 seconds
+}
+
+constexpr int MBS[3] = {1, 2, 4};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Crude per-step cost of one workgroup in cycles: matrix-core time at half of
+// peak against operand traffic at 64 B/clk, plus a fixed cost per tile.
+double tile_cost(int ntiles, int BM, int NT, int K, size_t es, bool w_lds, int B)
+{
+    const int rows = BM < B ? BM : B;
+    const double mfma = (double)ntiles * 2.0 * BM * NT * K / (4096.0 * 0.5);
+    double bytes = (double)ntiles * rows * K * (double)es;
+    if (!w_lds) bytes += (double)ntiles * NT * K * (double)es;
+    const double mem = bytes / 64.0;
+    return (mfma > mem ? mfma : mem) + 800.0 * ntiles;
+}
+
+}  // namespace
+
+bool plan_forward(DType t, const RecShape &sh, int num_cus, RecTiling *out)
+{
+    device_limits();
+    const size_t es = dsize(t);
+    const int Hr = sh.Hp ? sh.Hp : sh.H;
+    const int KC = (int)(64 / es);
+    bool found = false;
+    double best = 0;
+    for (int nbwi = 0; nbwi < 3; ++nbwi) {
+        const int NBW = 1 << nbwi, HN = 8 * NBW, NT = 32 * NBW;
+        const int nHT = (sh.H + HN - 1) / HN;
+        if (nHT > num_cus) continue;
+        for (int mbi = 0; mbi < 3; ++mbi) {
+            const int BM = 16 * MBS[mbi];
+            const int nBT = (sh.B + BM - 1) / BM;
+            const int bgroups = std::min(nBT, num_cus / nHT);
+            const int G = nHT * bgroups;
+            const int kpitch = (int)(round_up((size_t)Hr, KC) * es + 16);
+            const size_t zb = 2u * BM * NT * 4;
+            const size_t with_r = zb + (size_t)NT * kpitch;
+            const bool r_lds = with_r <= (size_t)g_lds_limit - 1024;
+            const size_t lds = r_lds ? with_r : (zb > 4096 ? zb : 4096);
+            if (lds > (size_t)g_lds_limit - 1024) continue;
+            const int per = (nBT + bgroups - 1) / bgroups;
+            double cost = tile_cost(per, BM, NT, Hr, es, r_lds, sh.B);
+            if (sh.Hp) cost += 2.0 * sh.B * sh.Hp * (double)sh.H / (4096.0 * 0.25 * G);
+            if (!found || cost < best) {
+                found = true;
+                best = cost;
+                *out = RecTiling{HN, BM, nHT, nBT, G, bgroups, nbwi * 3 + mbi, lds};
+                out->variant |= (r_lds ? 1 : 0) << 8;
+            }
+        }
+    }
+    return found;
+}
+
+bool plan_backward(DType t, const RecShape &sh, int num_cus, RecTiling *out)
+{
+    device_limits();
+    const size_t es = dsize(t);
+    const int KC = (int)(64 / es);
+    const int Kw = sh.Hp ? sh.Hp : 4 * sh.H;
+    bool found = false;
+    double best = 0;
+    for (int nbwi = 0; nbwi < 3; ++nbwi) {
+        const int HN = 8 << nbwi;
+        const int NBW = HN <= 16 ? 1 : 2, NT = 16 * NBW;
+        const int nHT = (sh.H + HN - 1) / HN;
+        if (nHT > num_cus) continue;
+        for (int mbi = 0; mbi < 3; ++mbi) {
+            const int BM = 16 * MBS[mbi];
+            const int nBT = (sh.B + BM - 1) / BM;
+            const int bgroups = std::min(nBT, num_cus / nHT);
+            const int G = nHT * bgroups;
+            const int kpitch = (int)(round_up((size_t)Kw, KC) * es + 16);
+            const size_t red = std::max<size_t>(4u * BM * NT * 4, 4096);
+            const size_t with_w = red + (size_t)NT * kpitch;
+            const bool w_lds = with_w <= (size_t)g_lds_limit - 1024;
+            const size_t lds = w_lds ? with_w : red;
+            if (lds > (size_t)g_lds_limit - 1024) continue;
+            const int per = (nBT + bgroups - 1) / bgroups;
+            double cost = tile_cost(per, BM, NT, Kw, es, w_lds, sh.B);
+            if (sh.Hp) cost += 2.0 * sh.B * sh.Hp * 4.0 * sh.H / (4096.0 * 0.25 * G);
+            if (!found || cost < best) {
+                found = true;
+                best = cost;
+                *out = RecTiling{HN, BM, nHT, nBT, G, bgroups, nbwi * 3 + mbi, lds};
+                out->variant |= (w_lds ? 1 : 0) << 8;
+            }
+        }
+    }
+    return found;
+}
+
+namespace {
+
+template <typename K>
+hipError_t coop_launch(K kernel, int grid, size_t lds, hipStream_t s, void *argp)
+{
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    void *args[] = {argp};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(kernel), dim3(grid), dim3(WGT), args,
+                                      (unsigned)lds, s);
+}
+
+template <typename TI>
+hipError_t fwd_dispatch(int variant, int grid, size_t lds, hipStream_t s, FwdArgs *a)
+{
+    switch (variant & 0xff) {
+    case 0: return coop_launch(lstm_fwd_kernel<TI, 1, 1>, grid, lds, s, a);
+    case 1: return coop_launch(lstm_fwd_kernel<TI, 2, 1>, grid, lds, s, a);
+    case 2: return coop_launch(lstm_fwd_kernel<TI, 4, 1>, grid, lds, s, a);
+    case 3: return coop_launch(lstm_fwd_kernel<TI, 1, 2>, grid, lds, s, a);
+    case 4: return coop_launch(lstm_fwd_kernel<TI, 2, 2>, grid, lds, s, a);
+    case 5: return coop_launch(lstm_fwd_kernel<TI, 4, 2>, grid, lds, s, a);
+    case 6: return coop_launch(lstm_fwd_kernel<TI, 1, 4>, grid, lds, s, a);
+    case 7: return coop_launch(lstm_fwd_kernel<TI, 2, 4>, grid, lds, s, a);
+    case 8: return coop_launch(lstm_fwd_kernel<TI, 4, 4>, grid, lds, s, a);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <typename TI, bool PROJ>
+hipError_t bwd_dispatch(int variant, int grid, size_t lds, hipStream_t s, BwdArgs *a)
+{
+    switch (variant & 0xff) {
+    case 0: return coop_launch(lstm_bwd_kernel<TI, 1, 1, PROJ>, grid, lds, s, a);
+    case 1: return coop_launch(lstm_bwd_kernel<TI, 2, 1, PROJ>, grid, lds, s, a);
+    case 2: return coop_launch(lstm_bwd_kernel<TI, 4, 1, PROJ>, grid, lds, s, a);
+    case 3: return coop_launch(lstm_bwd_kernel<TI, 1, 1, PROJ>, grid, lds, s, a);
+    case 4: return coop_launch(lstm_bwd_kernel<TI, 2, 1, PROJ>, grid, lds, s, a);
+    case 5: return coop_launch(lstm_bwd_kernel<TI, 4, 1, PROJ>, grid, lds, s, a);
+    case 6: return coop_launch(lstm_bwd_kernel<TI, 1, 2, PROJ>, grid, lds, s, a);
+    case 7: return coop_launch(lstm_bwd_kernel<TI, 2, 2, PROJ>, grid, lds, s, a);
+    case 8: return coop_launch(lstm_bwd_kernel<TI, 4, 2, PROJ>, grid, lds, s, a);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_forward(DType t, const RecShape &sh, const RecTiling &tl, const FwdBufs &bf, hipStream_t s)
+{
+    device_limits();
+    const size_t es = dsize(t);
+    const int Hr = sh.Hp ? sh.Hp : sh.H;
+    FwdArgs a;
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.Hp = sh.Hp; a.Hr = Hr; a.reverse = sh.reverse; a.ldy = sh.ldy;
+    a.R = static_cast<const char *>(bf.R);
+    a.P = static_cast<const char *>(bf.P);
+    a.h0 = static_cast<const char *>(bf.h0);
+    a.c0 = bf.c0;
+    a.gates = bf.gates; a.cs = bf.cs;
+    a.ms = static_cast<char *>(bf.ms);
+    a.y = static_cast<char *>(bf.y);
+    a.hT = static_cast<char *>(bf.hT);
+    a.cT = bf.cT;
+    a.sync = bf.sync;
+    a.timeout = g_timeout_ticks;
+    a.HN = tl.HN; a.nHT = tl.nHT; a.nBT = tl.nBT; a.bgroups = tl.bgroups;
+    a.r_lds = (tl.variant >> 8) & 1;
+    a.kpitch = (int)(round_up((size_t)Hr, 64 / es) * es + 16);
+
+    hipError_t e = fill_u32(bf.sync, SYNC_WORDS, 0u, s);   // barrier counter and abort flag
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    const double flops = 2.0 * sh.T * sh.B * G4 * Hr + (sh.Hp ? 2.0 * sh.T * sh.B * sh.H * sh.Hp : 0.0);
+    const double bytes = (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 4.0 + Hr * (double)es + (sh.Hp ? sh.H * (double)es : 0.0)) +
+                         G4 * Hr * (double)es + (sh.Hp ? (double)sh.Hp * sh.H * es : 0.0);
+    ProfScope ps(K_REC_FWD, s, flops, bytes);
+    return t == DType::BF16 ? fwd_dispatch<bf16_t>(tl.variant, tl.G, tl.lds, s, &a)
+                            : fwd_dispatch<float>(tl.variant, tl.G, tl.lds, s, &a);
+}
+
+hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, const BwdBufs &bf, hipStream_t s)
+{
+    device_limits();
+    const size_t es = dsize(t);
+    const int Hr = sh.Hp ? sh.Hp : sh.H;
+    BwdArgs a;
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.Hp = sh.Hp; a.Hr = Hr; a.reverse = sh.reverse; a.ldy = sh.ldy;
+    a.Rt = static_cast<const char *>(bf.Rt);
+    a.Pt = static_cast<const char *>(bf.Pt);
+    a.dy = static_cast<const char *>(bf.dy);
+    a.dhT = static_cast<const char *>(bf.dhT);
+    a.dcT = bf.dcT; a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
+    a.dz = static_cast<char *>(bf.dz);
+    a.dH = static_cast<char *>(bf.dH);
+    a.dh0 = static_cast<char *>(bf.dh0);
+    a.dc0 = bf.dc0;
+    a.dcn = bf.dcn; a.dhn = bf.dhn;
+    a.sync = bf.sync;
+    a.timeout = g_timeout_ticks;
+    a.HN = tl.HN; a.nHT = tl.nHT; a.nBT = tl.nBT; a.bgroups = tl.bgroups;
+    a.w_lds = (tl.variant >> 8) & 1;
+    const int Kw = sh.Hp ? sh.Hp : 4 * sh.H;
+    a.kpitch = (int)(round_up((size_t)Kw, 64 / es) * es + 16);
+
+    hipError_t e = fill_u32(bf.sync, SYNC_WORDS, 0u, s);
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    const double flops = 2.0 * sh.T * sh.B * G4 * Hr + (sh.Hp ? 2.0 * sh.T * sh.B * sh.H * sh.Hp : 0.0);
+    const double bytes = (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 8.0 + G4 * (double)es + Hr * (double)es) +
+                         G4 * Hr * (double)es + (sh.Hp ? (double)sh.Hp * sh.H * es : 0.0);
+    ProfScope ps(K_REC_BWD, s, flops, bytes);
+    if (t == DType::BF16)
+        return sh.Hp ? bwd_dispatch<bf16_t, true>(tl.variant, tl.G, tl.lds, s, &a)
+                     : bwd_dispatch<bf16_t, false>(tl.variant, tl.G, tl.lds, s, &a);
+    return sh.Hp ? bwd_dispatch<float, true>(tl.variant, tl.G, tl.lds, s, &a)
+                 : bwd_dispatch<float, false>(tl.variant, tl.G, tl.lds, s, &a);
+}
+
+hipError_t watchdog_read_and_clear(unsigned *tripped)
+{
+    unsigned v = 0;
+    hipError_t e = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_watchdog_tripped), sizeof(v), 0, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    *tripped = v;
+    if (v) {
+        const unsigned zero = 0;
+        e = hipMemcpyToSymbol(HIP_SYMBOL(g_watchdog_tripped), &zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+    }
+    return e;
+}
+
+}  // namespace lstm355

@@ -1,0 +1,96 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+
+import pytest
+
+from paper_1907_13257_amd import lstm355 as L
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = L.header_functions()
+    assert {"lstm_create", "lstm_forward", "lstm_backward", "lstm_destroy"} <= set(names)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(lib):
+    for s, name in enumerate(["LSTM_OK", "LSTM_ERR_INVALID_ARG", "LSTM_ERR_UNSUPPORTED", "LSTM_ERR_WORKSPACE",
+                              "LSTM_ERR_HIP", "LSTM_ERR_TIMEOUT"]):
+        assert L.lstm_status_string(s) == name
+    assert L.lstm_status_string(99) == "LSTM_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("kw", [
+    dict(T=0), dict(B=0), dict(I=0), dict(H=-8), dict(Hp=-8),
+    dict(I=12), dict(H=20), dict(Hp=4),
+    dict(ldx=8), dict(ldx=36), dict(ldy=8),
+])
+def test_create_rejects_bad_descriptors(lib, kw):
+    args = dict(T=4, B=3, I=32, H=16, Hp=0, dtype="bf16", reverse=False, ldx=0, ldy=0)
+    args.update(kw)
+    with pytest.raises(L.LSTMError) as e:
+        L.lstm_create(**args)
+    assert e.value.status == L.LSTM_ERR_INVALID_ARG
+
+
+def test_create_rejects_bad_dtype_and_reverse(lib):
+    h = ctypes.c_void_p()
+    d = L.lstm_desc_t(4, 3, 32, 16, 0, 7, 0, 0, 0)
+    assert lib.lstm_create(ctypes.byref(d), ctypes.byref(h)) == L.LSTM_ERR_INVALID_ARG
+    d = L.lstm_desc_t(4, 3, 32, 16, 0, 1, 2, 0, 0)
+    assert lib.lstm_create(ctypes.byref(d), ctypes.byref(h)) == L.LSTM_ERR_INVALID_ARG
+    assert lib.lstm_create(None, ctypes.byref(h)) == L.LSTM_ERR_INVALID_ARG
+
+
+def test_sizes_and_destroy(lib):
+    T, B, I, H = 5, 3, 16, 24
+    h = L.lstm_create(T, B, I, H, 0, "bf16")
+    # reserve holds fp32 gates [T][B][4H] and cells [T][B][H]
+    assert L.lstm_reserve_size(h) >= T * B * 4 * H * 4 + T * B * H * 4
+    # workspace holds at least the bf16 gate gradients [T][B][4H]
+    assert L.lstm_workspace_size(h) >= T * B * 4 * H * 2
+    hp = L.lstm_create(T, B, I, H, 8, "f32")
+    assert L.lstm_reserve_size(hp) >= T * B * 4 * H * 4 + T * B * H * 4 + T * B * H * 4
+    L.lstm_destroy(h)
+    L.lstm_destroy(hp)
+    assert lib.lstm_destroy(None) == L.LSTM_OK
+    assert lib.lstm_reserve_size(None) == 0
+
+
+def test_forward_backward_validate_before_launch(lib):
+    h = L.lstm_create(4, 3, 32, 16, 0, "bf16")
+    A = 1 << 20  # a 16-byte aligned stand-in address; validation fails before any use
+    # missing required pointers
+    assert lib.lstm_forward(h, None, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    # P given to a plain LSTM
+    assert lib.lstm_forward(h, A, None, None, A, A, A, A, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    # misaligned activation pointer
+    assert lib.lstm_forward(h, A + 2, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert "aligned" in L.lstm_last_error_detail()
+    # backward: missing weight gradients, bad accumulate flag
+    args = [A, None, None, A, None, None, A, A, None, A, A, None, None, None, A, A, A, None]
+    assert lib.lstm_backward(h, *args[:14], None, A, A, None, 0, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert lib.lstm_backward(h, *args, 2, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert lib.lstm_forward(None, A, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    hp = L.lstm_create(4, 3, 32, 16, 8, "bf16")
+    args_p = [A, None, None, A, None, None, A, A, A, A, A, None, None, None, A, A, A, None]
+    assert lib.lstm_backward(hp, *args_p, 0, A, None) == L.LSTM_ERR_INVALID_ARG   # dP missing
+    L.lstm_destroy(h)
+    L.lstm_destroy(hp)
+
+
+def test_add_validates(lib):
+    assert lib.lstm_add(5, 4, 1 << 20, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG
+    assert lib.lstm_add(1, 4, None, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG
+    assert lib.lstm_add(1, 0, None, None, None, None) == L.LSTM_OK
+
+
+def test_profile_api_without_records(lib):
+    L.lstm_profile_reset()
+    assert L.lstm_profile_read() == {}

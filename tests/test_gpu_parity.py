@@ -1,0 +1,206 @@
+"""GPU parity through the C ABI against the fp64 oracle, element by element,
+on sizes that span several tiles with ragged tails.
+
+Tolerances (normwise per tensor, max|a-r| / max|r|): fp32 mode 1e-4 on
+everything; bf16 mode 2e-2 on outputs and 5e-2 on gradients (input and
+weight gradients alike)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _gpu_helpers import TOL, announce, compare, normwise, run_oracle, run_stack_gpu, to_dev, to_f64
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def layer_case(T, B, I, H, Hp=0, dtype="bf16", reverse=False, seed=0, states=True, final_grads=True, scale=0.3):
+    """Draws one layer problem; returns host f64 arrays and device tensors."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    Hr = Hp if Hp else H
+
+    def T_(a):
+        return synth.Tensor(a, dtype)
+
+    c = dict(
+        x=T_(rng.standard_normal((T, B, I))),
+        W=T_(rng.uniform(-scale, scale, (4 * H, I))),
+        R=T_(rng.uniform(-scale, scale, (4 * H, Hr))),
+        b=rng.uniform(-scale, scale, 4 * H).astype(np.float32),
+        P=T_(rng.uniform(-scale, scale, (Hp, H))) if Hp else None,
+        h0=T_(rng.uniform(-1, 1, (B, Hr))) if states else None,
+        c0=rng.uniform(-1, 1, (B, H)).astype(np.float32) if states else None,
+        dy=T_(rng.standard_normal((T, B, Hr))),
+        dhT=T_(rng.standard_normal((B, Hr))) if final_grads else None,
+        dcT=rng.standard_normal((B, H)).astype(np.float32) if final_grads else None,
+    )
+    return c
+
+
+def f64(v):
+    if v is None:
+        return None
+    return v.f64 if isinstance(v, synth.Tensor) else v.astype(np.float64)
+
+
+def run_layer_gpu(c, T, B, I, H, Hp, dtype, reverse, accumulate_into=None):
+    from paper_1907_13257_amd import Layer
+    Hr = Hp if Hp else H
+    lay = Layer(T, B, I, H, Hp, dtype, reverse)
+    d = {k: to_dev(v) for k, v in c.items()}
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = torch.empty((T, B, Hr), dtype=td, device="cuda")
+    hT = torch.empty((B, Hr), dtype=td, device="cuda")
+    cT = torch.empty((B, H), dtype=torch.float32, device="cuda")
+    lay.forward(d["x"], d["W"], d["R"], d["b"], d["P"], d["h0"], d["c0"], y, hT, cT)
+    grads = dict(dW=torch.empty((4 * H, I), dtype=torch.float32, device="cuda"),
+                 dR=torch.empty((4 * H, Hr), dtype=torch.float32, device="cuda"),
+                 db=torch.empty((4 * H,), dtype=torch.float32, device="cuda"))
+    if Hp:
+        grads["dP"] = torch.empty((Hp, H), dtype=torch.float32, device="cuda")
+    if accumulate_into is not None:
+        for k in grads:
+            grads[k].copy_(torch.from_numpy(accumulate_into[k].astype(np.float32)))
+    dx = torch.empty((T, B, I), dtype=td, device="cuda")
+    dh0 = torch.empty((B, Hr), dtype=td, device="cuda")
+    dc0 = torch.empty((B, H), dtype=torch.float32, device="cuda")
+    lay.backward(d["dy"], d["x"], d["W"], d["R"], y, grads, P=d["P"], h0=d["h0"], c0=d["c0"], dhT=d["dhT"],
+                 dcT=d["dcT"], dx=dx, dh0=dh0, dc0=dc0, accumulate=accumulate_into is not None)
+    assert lay.check() == 0
+    torch.cuda.synchronize()
+    out = dict(y=to_f64(y), hT=to_f64(hT), cT=to_f64(cT), dx=to_f64(dx), dh0=to_f64(dh0), dc0=to_f64(dc0))
+    out.update({k: to_f64(v) for k, v in grads.items()})
+    out["tiling"] = lay.tiling()
+    lay.close()
+    return out
+
+
+def oracle_layer(c, Hp, reverse):
+    o = oracle.layer_forward(f64(c["x"]), f64(c["W"]), f64(c["R"]), f64(c["b"]), f64(c["P"]), f64(c["h0"]),
+                             f64(c["c0"]), reverse=reverse)
+    g = oracle.layer_backward(f64(c["x"]), f64(c["W"]), f64(c["R"]), f64(c["b"]), f64(c["dy"]), f64(c["P"]),
+                              f64(c["h0"]), f64(c["c0"]), f64(c["dhT"]), f64(c["dcT"]), reverse=reverse)
+    return dict(o, **g)
+
+
+def check_layer(gpu, ref, dtype, label):
+    tol = TOL[dtype]
+    errs = {}
+    for k in ("y", "hT", "cT"):
+        errs[k] = normwise(gpu[k], ref[k])
+    for k in ("dx", "dh0", "dc0", "dW", "dR", "db", "dP"):
+        if k in ref and k in gpu:
+            errs[k] = normwise(gpu[k], ref[k])
+    announce(f"{label} tiling={gpu.get('tiling')} " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    bad = {k: v for k, v in errs.items() if v > (tol["out"] if k in ("y", "hT", "cT") else tol["grad"])}
+    assert not bad, f"{label}: {bad}"
+
+
+LAYER_CASES = [
+    # (T, B, I, H, Hp, dtype, reverse)
+    (8, 4, 32, 64, 0, "f32", False),       # the tiny config's shape in fp32
+    (8, 4, 32, 64, 0, "bf16", False),
+    (5, 37, 40, 72, 0, "f32", False),      # ragged batch, hidden and input tails
+    (5, 37, 40, 72, 0, "bf16", True),
+    (7, 50, 136, 200, 0, "bf16", False),   # several hidden tiles, K chunks with a tail
+    (6, 19, 24, 48, 16, "f32", False),     # LSTMP
+    (6, 33, 48, 136, 40, "bf16", True),    # LSTMP reverse, ragged
+    (3, 130, 64, 96, 0, "bf16", False),    # more batch tiles than one workgroup row
+    (1, 3, 16, 16, 0, "f32", False),       # a single step
+]
+
+
+@pytest.mark.parametrize("T,B,I,H,Hp,dtype,reverse", LAYER_CASES)
+def test_layer_parity(T, B, I, H, Hp, dtype, reverse):
+    label = f"layer T{T} B{B} I{I} H{H} Hp{Hp} {dtype} rev{int(reverse)}"
+    announce(label)
+    c = layer_case(T, B, I, H, Hp, dtype, reverse, seed=T * 1000 + B)
+    gpu = run_layer_gpu(c, T, B, I, H, Hp, dtype, reverse)
+    ref = oracle_layer(c, Hp, reverse)
+    check_layer(gpu, ref, dtype, label)
+
+
+def test_layer_without_initial_state_or_final_grads():
+    T, B, I, H = 6, 9, 32, 40
+    announce("layer zero states")
+    c = layer_case(T, B, I, H, 0, "f32", False, seed=5, states=False, final_grads=False)
+    gpu = run_layer_gpu(c, T, B, I, H, 0, "f32", False)
+    ref = oracle_layer(c, 0, False)
+    check_layer(gpu, ref, "f32", "zero states")
+
+
+def test_gradient_accumulation():
+    """accumulate=1 adds this mini-batch's weight gradients to the buffers."""
+    T, B, I, H = 4, 6, 16, 24
+    announce("accumulate")
+    c = layer_case(T, B, I, H, 8, "f32", False, seed=6)
+    rng = np.random.default_rng(1)
+    prior = dict(dW=rng.standard_normal((4 * H, I)), dR=rng.standard_normal((4 * H, 8)),
+                 db=rng.standard_normal(4 * H), dP=rng.standard_normal((8, H)))
+    prior = {k: v.astype(np.float32).astype(np.float64) for k, v in prior.items()}
+    gpu = run_layer_gpu(c, T, B, I, H, 8, "f32", False, accumulate_into=prior)
+    ref = oracle_layer(c, 8, False)
+    for k in ("dW", "dR", "db", "dP"):
+        assert normwise(gpu[k], ref[k] + prior[k]) <= 1e-4, k
+
+
+def test_tiny_config_parity_fp32_and_bf16():
+    for dtype in ("f32", "bf16"):
+        wl = synth.tiny(dtype)
+        announce(f"tiny config {dtype}")
+        prob = synth.draw(wl)
+        # the tiny config carries initial states: run it as a single layer
+        p = prob.params[0][0]
+        c = dict(x=prob.x, W=p.W, R=p.R, b=p.b, P=None, h0=prob.h0[0][0], c0=prob.c0[0][0], dy=prob.dy,
+                 dhT=None, dcT=None)
+        gpu = run_layer_gpu(c, wl.T, wl.B, 32, 64, 0, dtype, False)
+        ref = oracle_layer(c, 0, False)
+        check_layer(gpu, ref, dtype, f"tiny {dtype}")
+
+
+def small_stack_workload(dtype="bf16"):
+    layers = [synth.LayerSpec(48, 32, bidirectional=True), synth.LayerSpec(64, 40),
+              synth.LayerSpec(40, 40, residual=True), synth.LayerSpec(40, 40, residual=True)]
+    return synth.Workload("small_stack", T=6, B=21, layers=layers, dtype=dtype, seed=9, w_scale=0.2)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_small_stack_parity(dtype):
+    wl = small_stack_workload(dtype)
+    announce(f"small stack {dtype}")
+    prob = synth.draw(wl)
+    gpu, _ = run_stack_gpu(prob)
+    ref = run_oracle(prob)
+    compare(gpu, ref, dtype, label=f"small stack {dtype}")
+
+
+def test_small_lstmp_stack_parity():
+    wl = synth.Workload("small_lstmp", T=5, B=20, layers=[synth.LayerSpec(32, 64, Hp=32), synth.LayerSpec(32, 64, Hp=32)],
+                        dtype="bf16", seed=10, w_scale=0.1)
+    announce("small lstmp stack")
+    prob = synth.draw(wl)
+    gpu, _ = run_stack_gpu(prob)
+    ref = run_oracle(prob)
+    compare(gpu, ref, "bf16", label="small lstmp stack")
+
+
+def test_deterministic():
+    """Two identical runs give bitwise-identical outputs and gradients."""
+    wl = small_stack_workload("bf16")
+    announce("determinism")
+    prob = synth.draw(wl)
+    a, stack = run_stack_gpu(prob)
+    b, _ = run_stack_gpu(prob, stack=stack)
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["dx"], b["dx"])
+    for la, lb in zip(a["layers"], b["layers"]):
+        for ga, gb in zip(la, lb):
+            for k in ga:
+                assert np.array_equal(ga[k], gb[k]), k
