@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Throughput of the per-worker LSTM training step (forward + BPTT + all
+gradients) on one MI355X.
+
+Default workload: the GNMT-shaped encoder stack of 4 unidirectional LSTM
+layers, input 1024, hidden 1024, T=50, mini-batch B=128, bf16 storage with
+fp32 accumulation (the headline configuration).  Inputs are seeded synthetic
+tensors already resident in HBM when timing starts.
+
+Prints one JSON line.  `value` is FLOP/s of the whole step (2*M*N*K over
+every matrix product of forward, BPTT and gradients) in TFLOP/s.
+`roofline` describes the kernel class with the largest share of the timed
+region, timed with HIP events the library records around each launch on
+the stream it runs on.  `cpu_baseline` times the fp64 oracle on a bounded
+sample of the same workload (a subset of the batch rows) on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix / vector peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+GEMM_CLASSES = ("gemm_input_proj", "gemm_dx", "gemm_dw", "gemm_dr", "gemm_dp")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1907_13257_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def make_workload(args):
+    import synth
+    if args.workload == "gnmt4":
+        return synth.gnmt4(B=args.batch or 128, seed=1 if not args.batch or args.batch == 128 else 2)
+    if args.workload == "biglstm":
+        return synth.biglstm(B=args.batch or 128)
+    if args.workload == "gnmt8":
+        return synth.gnmt8(B=args.batch or 256)
+    raise SystemExit(f"unknown workload {args.workload}")
+
+
+def workload_name(wl) -> str:
+    L0 = wl.layers[0]
+    kinds = {"gnmt4": "gnmt4_lstm", "biglstm": "biglstm_lstmp", "gnmt8": "gnmt8_bi_residual_lstm"}
+    base = kinds.get(wl.name.split("_B")[0], wl.name)
+    hp = f"_P{L0.Hp}" if L0.Hp else ""
+    return f"{base}_L{len(wl.layers)}_I{L0.I}_H{L0.H}{hp}_T{wl.T}_B{wl.B}"
+
+
+def cpu_baseline(wl, rows: int):
+    """The oracle, untuned, on the first `rows` batch rows of the same
+    workload (rows are independent, so the work per row is the full
+    problem's); reported in the same unit as `value`."""
+    import numpy as np
+    import oracle
+    import synth
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from _gpu_helpers import oracle_layers
+
+    prob = synth.draw(wl)
+    sel = np.arange(min(rows, wl.B))
+    layers = oracle_layers(prob)
+    x = prob.x.f64[:, sel]
+    dy = prob.dy.f64[:, sel]
+    t0 = time.perf_counter()
+    oracle.stack_forward(x, layers)
+    oracle.stack_backward(x, layers, dy)
+    dt = time.perf_counter() - t0
+    frac = len(sel) / wl.B
+    flops = wl.gemm_flops() * frac
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{len(sel)} of {wl.B} batch rows of the same stack (all layers, all {wl.T} steps), "
+                      f"forward + backward, fp64; {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gnmt4", choices=["gnmt4", "biglstm", "gnmt8"])
+    ap.add_argument("--batch", type=int, default=0)
+    ap.add_argument("--cpu-rows", type=int, default=16, help="batch rows for the oracle baseline (0: skip)")
+    ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="only run a plain torch copy of this many MiB (counter calibration) and exit")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the data-parallel all-reduce is out of scope); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_each_way": n * 4, "launches": 5}))
+        return
+
+    import synth
+    from paper_1907_13257_amd import Stack, lstm355
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from _gpu_helpers import device_params, stack_layers, to_dev
+
+    wl = make_workload(args)
+    prob = synth.draw(wl)
+    stack = Stack(wl.T, wl.B, stack_layers(wl), wl.dtype)
+    params = device_params(prob)
+    grads = stack.alloc_grads(params)
+    x = to_dev(prob.x)
+    dy = to_dev(prob.dy)
+    tiling = [L.tiling() for L in stack.dirs[0]]
+
+    def step():
+        stack.forward(x, params)
+        stack.backward(dy, params, grads)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    st = stack.check()
+    if st != 0:
+        raise SystemExit(f"watchdog tripped during warmup ({lstm355.lstm_status_string(st)})")
+
+    # uninstrumented timing
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_plain = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # timed region with per-kernel events
+    prof = not args.no_profile
+    if prof:
+        lstm355.lstm_profile_reset()
+        lstm355.lstm_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    stats = {}
+    if prof:
+        lstm355.lstm_profile_enable(False)
+        stats = lstm355.lstm_profile_read()
+        lstm355.lstm_profile_reset()
+    st = stack.check()
+    if st != 0:
+        raise SystemExit(f"watchdog tripped ({lstm355.lstm_status_string(st)})")
+
+    flops = wl.gemm_flops()
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    tflops = flops / (ms / 1e3) / 1e12
+
+    kernels = {}
+    for name, s in stats.items():
+        avg = s["total_ms"] / s["launches"]
+        kernels[name] = dict(launches_per_step=s["launches"] / args.steps, ms_per_step=s["total_ms"] / args.steps,
+                             avg_launch_ms=avg,
+                             tflops=(s["flops"] / s["launches"]) / (avg / 1e3) / 1e12 if avg > 0 else None,
+                             gbs=(s["bytes"] / s["launches"]) / (avg / 1e3) / 1e9 if avg > 0 else None)
+    roofline = None
+    gemm_summary = None
+    if stats:
+        dom = max(stats, key=lambda k: stats[k]["total_ms"])
+        s = stats[dom]
+        avg_s = s["total_ms"] / s["launches"] / 1e3
+        traffic = None
+        if os.path.exists(TRAFFIC_FILE):
+            with open(TRAFFIC_FILE) as f:
+                tr = json.load(f)
+            ent = tr.get("kernels", {}).get(dom)
+            if ent and tr.get("source_hash") == kernel_source_hash() and tr.get("workload") == workload_name(wl):
+                traffic = ent.get("hbm_bytes_per_launch")
+        if dom in GEMM_CLASSES or dom.startswith("recurrent"):
+            # recurrent kernels run their dependent products on the matrix
+            # cores too, but are bound by the per-step barrier and traffic;
+            # they are reported against HBM with their algorithmic bytes.
+            pass
+        if dom in GEMM_CLASSES:
+            ach = s["flops"] / s["launches"] / avg_s / 1e12
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                        "frac": ach / peak, "traffic": traffic}
+        else:
+            ach = s["bytes"] / s["launches"] / avg_s / 1e9
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+        gf = sum(stats[k]["flops"] for k in GEMM_CLASSES if k in stats)
+        gt = sum(stats[k]["total_ms"] for k in GEMM_CLASSES if k in stats)
+        if gt > 0:
+            g_tf = gf / (gt / 1e3) / 1e12
+            gemm_summary = {"tflops": g_tf, "frac_of_peak": g_tf / peak, "ms_per_step": gt / args.steps}
+
+    cpu = None
+    if args.cpu_rows:
+        cpu = cpu_baseline(wl, args.cpu_rows)
+
+    out = {
+        "metric": "LSTM fwd+BPTT ms/step and TFLOP/s (% bf16 MFMA peak), 4x1024 B=128 T=50",
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "ms_per_step_without_kernel_events": ms_plain,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded; x, dy ~ N(0,1), weights ~ U(-a,a))",
+        "config": {"workload": workload_name(wl), "layers": len(wl.layers), "T": wl.T, "B": wl.B,
+                   "I": wl.layers[0].I, "H": wl.layers[0].H, "Hp": wl.layers[0].Hp,
+                   "step_gflop": flops / 1e9, "parallelism": "single GPU (per-worker step)"},
+        "frac_of_peak_whole_step": tflops / peak,
+        "gemm": gemm_summary,
+        "roofline": roofline,
+        "kernels": kernels,
+        "tiling_layer0": tiling,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -130,7 +130,9 @@ const char *lstm_last_error_detail(void);
 /* Diagnostics: the tiling chosen for this handle on the current device.
  * out8 = {fwd workgroups, fwd cells per workgroup, fwd batch rows per tile,
  * fwd variant, bwd workgroups, bwd cells per workgroup, bwd batch rows per
- * tile, bwd variant}; a workgroup count of 0 means no tiling fits. */
+ * tile, bwd variant}; a workgroup count of 0 means no tiling fits.  Variant
+ * 1000 marks the XCD-local kernels (bf16, plain LSTM, H in {256, 512, 1024}:
+ * each XCD owns ceil(B/8) batch rows, each workgroup H/32 cells). */
 lstm_status_t lstm_describe_tiling(lstm_handle_t h, int *out8);
 
 /* Elementwise out[i] = a[i] + b[i] for i < n, in fp32 arithmetic, rounded to

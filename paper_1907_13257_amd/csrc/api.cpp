@@ -203,7 +203,10 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
         fb.ms = d.Hp ? rv + h->r_ms : nullptr;
         fb.y = y; fb.hT = hT; fb.cT = cT;
         fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
+        if (xcd_path_ok(h->dt, sh, h->num_cus))
+            TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s));
+        else
+            TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
         return LSTM_OK;
     } catch (...) {
         return invalid("exception");
@@ -259,7 +262,10 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         bb.dhn = reinterpret_cast<float *>(wv + h->w_dhn);
         bb.dh0 = dh0; bb.dc0 = dc0;
         bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
+        if (xcd_path_ok(h->dt, sh, h->num_cus))
+            TRY_HIP("backward recurrence (XCD-local)", launch_backward_xcd(sh, bb, watchdog_ticks(), s));
+        else
+            TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
 
         if (dx) {  // dX = dZ W
             GemmDesc g{};
@@ -326,7 +332,18 @@ extern "C" lstm_status_t lstm_check(lstm_handle_t h, void *workspace, void *stre
     hipStream_t s = static_cast<hipStream_t>(stream);
     TRY_HIP("stream sync", hipStreamSynchronize(s));
     unsigned tripped = 0;
+    unsigned tripped_xcd = 0;
     TRY_HIP("read watchdog flag", watchdog_read_and_clear(&tripped));
+    TRY_HIP("read watchdog flag", xcd_tripped_read_and_clear(&tripped_xcd));
+    tripped |= tripped_xcd;
+    if (tripped & TRIP_PLACEMENT) {
+        // workgroups were not spread over the XCDs as the XCD-local kernels
+        // require: stop using them in this process
+        xcd_path_disable();
+        std::snprintf(g_detail, sizeof(g_detail), "XCD-local kernel found a workgroup on an unexpected XCD; "
+                                                  "falling back to the generic kernels from now on");
+        return LSTM_ERR_UNSUPPORTED;
+    }
     if (tripped) {
         std::snprintf(g_detail, sizeof(g_detail), "a grid barrier's watchdog expired");
         return LSTM_ERR_TIMEOUT;
@@ -349,6 +366,14 @@ extern "C" lstm_status_t lstm_describe_tiling(lstm_handle_t h, int *out8)
     if (!h || !out8) return invalid("NULL pointer");
     lstm_status_t st = ensure_plan(h);
     if (st != LSTM_OK) return st;
+    RecShape sh{h->d.T, h->d.B, h->d.I, h->d.H, h->d.Hp, h->d.reverse, h->ldy};
+    if (xcd_path_ok(h->dt, sh, h->num_cus)) {
+        // XCD-local kernels: 256 workgroups, H/32 cells each, ceil(B/8) rows per XCD
+        const int rx = (h->d.B + 7) / 8;
+        const int v[8] = {256, h->d.H / 32, rx, XCD_VARIANT, 256, h->d.H / 32, rx, XCD_VARIANT};
+        for (int i = 0; i < 8; ++i) out8[i] = v[i];
+        return LSTM_OK;
+    }
     out8[0] = h->fwd_ok ? h->fwd.G : 0;
     out8[1] = h->fwd.HN;
     out8[2] = h->fwd.BM;

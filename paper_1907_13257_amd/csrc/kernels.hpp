@@ -112,11 +112,29 @@ struct BwdBufs {
 };
 hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, const BwdBufs &b, hipStream_t s);
 
-// Workspace layout of the sync block (bytes); zeroed before every launch.
-constexpr size_t SYNC_BYTES = 1024;
-constexpr int SYNC_COUNT0 = 0;     // u32 index of barrier counter
-constexpr int SYNC_ABORT = 64;     // u32 index of this launch's abort flag
-constexpr int SYNC_WORDS = 128;    // u32 words cleared before each launch
+// Workspace layout of the sync block (u32 words); the words a kernel uses are
+// zeroed before it is launched.
+constexpr size_t SYNC_BYTES = 4096;
+constexpr int SYNC_COUNT0 = 0;     // barrier counter of the generic kernels
+constexpr int SYNC_ABORT = 64;     // abort flag of the generic kernels
+constexpr int SYNC_WORDS = 128;    // words cleared before a generic launch
+constexpr int XCD_FLAGS = 256;     // per-workgroup step counters of the XCD-local kernels (256 words)
+constexpr int XCD_ABORT = 256;     // abort flag, relative to XCD_FLAGS
+constexpr int XCD_WORDS = 257;     // words cleared before an XCD-local launch
+
+// Sticky error bits of the library (device variable): 1 = a watchdog expired,
+// 2 = an XCD-local kernel found a workgroup on an unexpected XCD.
+constexpr unsigned TRIP_WATCHDOG = 1u, TRIP_PLACEMENT = 2u;
+
+// XCD-local recurrences (recurrent_xcd.hip): bf16, plain LSTM, H in {256,
+// 512, 1024}, exactly 256 CUs.
+bool xcd_path_ok(DType t, const RecShape &sh, int num_cus);
+constexpr int XCD_VARIANT = 1000;   // variant reported by lstm_describe_tiling for these kernels
+void xcd_path_disable();
+hipError_t xcd_tripped_read_and_clear(unsigned *tripped);   // like watchdog_read_and_clear
+unsigned long long watchdog_ticks();
+hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s);
+hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &b, unsigned long long timeout, hipStream_t s);
 
 // Reads (synchronously) and clears the library's sticky watchdog word on the
 // current device: nonzero if a grid barrier gave up since the last call.

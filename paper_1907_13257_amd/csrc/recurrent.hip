@@ -53,7 +53,7 @@ __device__ __forceinline__ bool grid_barrier(unsigned *sync, unsigned target, un
                 break;
             }
             if (wall_clock64() - t0 > timeout) {
-                __hip_atomic_store(&g_watchdog_tripped, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_or(&g_watchdog_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __hip_atomic_store(sync + SYNC_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 ab = 1;
                 break;
@@ -688,6 +688,12 @@ hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, con
                      : bwd_dispatch<bf16_t, false>(tl.variant, tl.G, tl.lds, s, &a);
     return sh.Hp ? bwd_dispatch<float, true>(tl.variant, tl.G, tl.lds, s, &a)
                  : bwd_dispatch<float, false>(tl.variant, tl.G, tl.lds, s, &a);
+}
+
+unsigned long long watchdog_ticks()
+{
+    device_limits();
+    return g_timeout_ticks;
 }
 
 hipError_t watchdog_read_and_clear(unsigned *tripped)

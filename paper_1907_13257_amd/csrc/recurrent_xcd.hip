@@ -1,0 +1,462 @@
+// recurrent_xcd.hip -- persistent forward / BPTT recurrences whose per-step
+// exchange stays inside one XCD (bf16, plain LSTM, H in {256, 512, 1024}).
+//
+// The MI355X has 8 XCDs of 32 CUs, each XCD with its own L2; a 256-workgroup
+// launch places workgroup w on XCD w % 8 (checked at run time against the
+// XCC_ID register).  XCD x owns batch rows [x*RX, x*RX + RX), RX = ceil(B/8),
+// and all H cells of those rows: its 32 workgroups each own HN = H/32 cells.
+// The rows of h_{t-1} (forward) and of dz_t (backward) that a workgroup needs
+// are therefore produced inside its own XCD and travel through that XCD's
+// L2 only.  Every workgroup keeps its share of the recurrent weights in
+// registers for the whole kernel: forward, the 4*HN rows of R feeding its
+// cells (256 KiB at H = 1024, 32 KiB per wave); backward, the HN columns of R
+// (rows of R^T).
+//
+// Exchange protocol per step (no grid barrier, no cache flushes):
+//   producer: plain stores of its cells of h_t (or dz_t) -> wait until every
+//             store of the workgroup has completed -> plain store of its step
+//             counter in the flag array;
+//   consumer: one wave polls the 32 step counters of its XCD with
+//             device-coherent (sc1) loads, which miss the CU's L1; then the
+//             workgroup loads the exchanged rows with plain loads.  Those
+//             addresses are written once per launch and never read before
+//             the step that consumes them, so the CU's L1 cannot hold a stale
+//             copy, and the XCD's L2 holds the producers' data.
+// Polling has a wall-clock watchdog and an abort flag, so every wave exits.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace lstm355 {
+
+// Sticky error bits of this translation unit's kernels (TRIP_* values).
+__device__ unsigned g_xcd_tripped = 0;
+
+namespace {
+
+constexpr int XT = 512;          // threads per workgroup (8 waves, 2 per SIMD)
+constexpr int NXCD = 8;
+constexpr int WG_PER_XCD = 32;
+constexpr int HWREG_XCC_ID = (31 << 11) | (0 << 6) | 20;   // s_getreg: XCC_ID, 32 bits
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, 0x7fffffff, 0x00020000);
+}
+
+// Wave 0 polls the step counters of the 32 workgroups of XCD `xcd` until all
+// reach `target`.  Returns false (for the whole workgroup) on abort/timeout.
+__device__ __forceinline__ bool wait_xcd(const unsigned *flags, int xcd, unsigned target, unsigned long long timeout,
+                                         int *s_ok)
+{
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        const __amdgpu_buffer_rsrc_t r = rsrc(flags);
+        const unsigned long long t0 = wall_clock64();
+        int ok = 1;
+        while (true) {
+            unsigned f = target;
+            if (lane < WG_PER_XCD) f = __builtin_amdgcn_raw_buffer_load_b32(r, (xcd * WG_PER_XCD + lane) * 4, 0, 16);
+            unsigned ab = 0;
+            if (lane == 32) ab = __builtin_amdgcn_raw_buffer_load_b32(r, XCD_ABORT * 4, 0, 16);
+            if (__builtin_amdgcn_ballot_w64(ab != 0)) {
+                ok = 0;
+                break;
+            }
+            if (__builtin_amdgcn_ballot_w64(f < target) == 0) break;
+            if (wall_clock64() - t0 > timeout) {
+                if (lane == 0) {
+                    __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(const_cast<unsigned *>(flags) + XCD_ABORT, 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                }
+                ok = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (lane == 0) *s_ok = ok;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
+// All of the workgroup's stores have completed, then its step counter is set.
+__device__ __forceinline__ void publish(unsigned *flags, int wg_index, unsigned value)
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) flags[wg_index] = value;
+}
+
+// Placement check: this workgroup must run on XCD blockIdx.x % 8.
+__device__ __forceinline__ bool placed_ok(unsigned *flags, int *s_ok)
+{
+    if (threadIdx.x == 0) {
+        const unsigned x = __builtin_amdgcn_s_getreg(HWREG_XCC_ID) & 0xfu;
+        int ok = x == (blockIdx.x & 7u);
+        if (!ok) {
+            __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_PLACEMENT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        *s_ok = ok;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
+struct XFwdArgs {
+    int T, B, H, reverse, RX;
+    long ldy;
+    const bf16_t *R, *h0;
+    const float *c0;
+    float *gates, *cs;
+    bf16_t *y, *hT;
+    float *cT;
+    unsigned *flags;
+    unsigned long long timeout;
+};
+
+// Waves: kq = wave & 3 takes a quarter of the k chunks, nh = wave >> 2 half
+// of the 4*HN gate rows.  MBX blocks of 16 batch rows per XCD.
+template <int HN, int MBX>
+__global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
+{
+    constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
+    constexpr int NBH = NT / 32;      // 16-row blocks per wave half
+    constexpr int KCW = HN / 4;       // 32-wide k chunks per wave (H/32 = HN chunks in all)
+    constexpr int NCELL = 16 * HN;    // cells of one row block
+    __shared__ float red[4][16][NT];
+    __shared__ int s_ok;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int kq = w & 3, nh = w >> 2;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int H = a.H, B = a.B;
+    const long G4 = 4L * H;
+    const int j0 = slot * HN;
+    const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
+
+    if (!placed_ok(a.flags, &s_ok)) return;
+
+    // resident weights: rows of R for this workgroup's cells, this wave's k range
+    u32x4 rf[NBH][KCW];
+#pragma unroll
+    for (int i = 0; i < NBH; ++i) {
+        const int n = (nh * NBH + i) * 16 + (lane & 15);
+        const int g = n / HN, u = n % HN;
+        const bf16_t *rrow = a.R + (long)(g * H + j0 + u) * H;
+#pragma unroll
+        for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + (kq * KCW + c) * 32 + (lane >> 4) * 8);
+    }
+
+    const bool has_cell = tid < NCELL;
+    const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
+    float creg[MBX];
+#pragma unroll
+    for (int mb = 0; mb < MBX; ++mb) {
+        const int b = row0 + mb * 16 + cr;
+        creg[mb] = (has_cell && b < rowend && a.c0) ? a.c0[(long)b * H + cj] : 0.0f;
+    }
+
+    int tprev = 0;
+    for (int s = 0; s < a.T; ++s) {
+        const int t = a.reverse ? a.T - 1 - s : s;
+        const bool last = s == a.T - 1;
+        // input projection of this step for the own cells (independent of h_{t-1})
+        float gx[MBX][4];
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + cr;
+            const bool v = has_cell && b < rowend;
+            const float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gx[mb][g] = v ? gp[g * H] : 0.0f;
+        }
+        const bf16_t *hp = a.h0;
+        long ldh = H;
+        if (s > 0) {
+            if (!wait_xcd(a.flags, xcd, (unsigned)s, a.timeout, &s_ok)) return;
+            hp = a.y + (long)tprev * B * a.ldy;
+            ldh = a.ldy;
+        }
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            f32x4 acc[NBH];
+#pragma unroll
+            for (int i = 0; i < NBH; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (hp) {
+                const int b = row0 + mb * 16 + (lane & 15);
+                u32x4 fa[KCW];
+#pragma unroll
+                for (int c = 0; c < KCW; ++c)
+                    fa[c] = b < rowend ? ldg16(hp + (long)b * ldh + (kq * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+#pragma unroll
+                for (int c = 0; c < KCW; ++c)
+#pragma unroll
+                    for (int i = 0; i < NBH; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
+            }
+#pragma unroll
+            for (int i = 0; i < NBH; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) red[kq][4 * (lane >> 4) + v][(nh * NBH + i) * 16 + (lane & 15)] = acc[i][v];
+            __syncthreads();
+            const int b = row0 + mb * 16 + cr;
+            if (has_cell && b < rowend) {
+                float z[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    z[g] = red[0][cr][g * HN + cu] + red[1][cr][g * HN + cu] + red[2][cr][g * HN + cu] +
+                           red[3][cr][g * HN + cu] + gx[mb][g];
+                const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+                const float c = fg * creg[mb] + ig * gg;
+                const float m = og * tanh_f(c);
+                creg[mb] = c;
+                float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+                gp[0] = ig;
+                gp[H] = fg;
+                gp[2 * H] = gg;
+                gp[3 * H] = og;
+                a.cs[((long)t * B + b) * H + cj] = c;
+                const bf16_t hv = f32_to_bf16(m);
+                a.y[((long)t * B + b) * a.ldy + cj] = hv;
+                if (last) {
+                    if (a.hT) a.hT[(long)b * H + cj] = hv;
+                    if (a.cT) a.cT[(long)b * H + cj] = c;
+                }
+            }
+            __syncthreads();
+        }
+        if (!last) publish(a.flags, xcd * WG_PER_XCD + slot, (unsigned)(s + 1));
+        tprev = t;
+    }
+}
+
+struct XBwdArgs {
+    int T, B, H, reverse, RX;
+    long ldy;
+    const bf16_t *Rt, *dy, *dhT;
+    const float *dcT, *c0, *gates, *cs;
+    bf16_t *dz, *dh0;
+    float *dc0;
+    unsigned *flags;
+    unsigned long long timeout;
+};
+
+// Waves split the 4H-long reduction of dh_{t-1} = R^T dz_t in eight.
+template <int HN, int MBX>
+__global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
+{
+    constexpr int NBB = HN >= 16 ? HN / 16 : 1;   // 16-column blocks of owned cells
+    constexpr int NC = 16 * NBB;
+    constexpr int KCW = HN / 2;                   // 32-wide k chunks per wave (4H/32 = 4*HN in all)
+    constexpr int NCELL = 16 * HN;
+    __shared__ float red[8][16][NC];
+    __shared__ int s_ok;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int H = a.H, B = a.B;
+    const long G4 = 4L * H;
+    const int j0 = slot * HN;
+    const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
+
+    if (!placed_ok(a.flags, &s_ok)) return;
+
+    // resident weights: rows of R^T (= columns of R) of the owned cells, this wave's k range
+    u32x4 rf[NBB][KCW];
+#pragma unroll
+    for (int i = 0; i < NBB; ++i) {
+        const int n = i * 16 + (lane & 15);
+        const bf16_t *rrow = a.Rt + (long)(j0 + (n < HN ? n : 0)) * G4;
+#pragma unroll
+        for (int c = 0; c < KCW; ++c)
+            rf[i][c] = n < HN ? ldg16(rrow + (w * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+    }
+
+    const bool has_cell = tid < NCELL;
+    const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
+    float dhn[MBX], dcn[MBX];
+#pragma unroll
+    for (int mb = 0; mb < MBX; ++mb) {
+        const int b = row0 + mb * 16 + cr;
+        const bool v = has_cell && b < rowend;
+        dhn[mb] = (v && a.dhT) ? to_f32(a.dhT[(long)b * H + cj]) : 0.0f;
+        dcn[mb] = (v && a.dcT) ? a.dcT[(long)b * H + cj] : 0.0f;
+    }
+
+    unsigned done = 0;
+    for (int s = a.T - 1; s >= 0; --s) {
+        const int t = a.reverse ? a.T - 1 - s : s;
+        const int tp = a.reverse ? t + 1 : t - 1;
+        // per-cell inputs of this step (independent of the recurrence)
+        float dyv[MBX], g4[MBX][4], cv[MBX], cpv[MBX];
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + cr;
+            const bool v = has_cell && b < rowend;
+            const long rt = (long)t * B + b;
+            dyv[mb] = v ? to_f32(a.dy[rt * a.ldy + cj]) : 0.0f;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) g4[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
+            cv[mb] = v ? a.cs[rt * H + cj] : 0.0f;
+            cpv[mb] = v ? (s > 0 ? a.cs[((long)tp * B + b) * H + cj] : (a.c0 ? a.c0[(long)b * H + cj] : 0.0f)) : 0.0f;
+        }
+        // gate gradients of the owned cells
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + cr;
+            if (has_cell && b < rowend) {
+                const float ig = g4[mb][0], fg = g4[mb][1], gg = g4[mb][2], og = g4[mb][3];
+                const float dm = dyv[mb] + dhn[mb];
+                const float tc = tanh_f(cv[mb]);
+                const float d_o = dm * tc;
+                const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
+                const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv[mb];
+                bf16_t *dzp = a.dz + ((long)t * B + b) * G4 + cj;
+                dzp[0] = f32_to_bf16(d_i * ig * (1.0f - ig));
+                dzp[H] = f32_to_bf16(d_f * fg * (1.0f - fg));
+                dzp[2 * H] = f32_to_bf16(d_g * (1.0f - gg * gg));
+                dzp[3 * H] = f32_to_bf16(d_o * og * (1.0f - og));
+                dcn[mb] = d_c * fg;
+                if (s == 0 && a.dc0) a.dc0[(long)b * H + cj] = dcn[mb];
+            }
+        }
+        if (s == 0 && !a.dh0) break;
+        publish(a.flags, xcd * WG_PER_XCD + slot, ++done);
+        if (!wait_xcd(a.flags, xcd, done, a.timeout, &s_ok)) return;
+        // dh_{t-1} for the owned cells: dz_t of this XCD's rows times the resident R^T rows
+        const bf16_t *dzt = a.dz + (long)t * B * G4;
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + (lane & 15);
+            u32x4 fa[KCW];
+#pragma unroll
+            for (int c = 0; c < KCW; ++c)
+                fa[c] = b < rowend ? ldg16(dzt + (long)b * G4 + (w * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+            f32x4 acc[NBB];
+#pragma unroll
+            for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < KCW; ++c)
+#pragma unroll
+                for (int i = 0; i < NBB; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
+#pragma unroll
+            for (int i = 0; i < NBB; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+            __syncthreads();
+            const int bc = row0 + mb * 16 + cr;
+            if (has_cell && bc < rowend) {
+                float v = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+                if (s > 0)
+                    dhn[mb] = v;
+                else
+                    a.dh0[(long)bc * H + cj] = f32_to_bf16(v);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+template <typename K>
+hipError_t coop512(K kernel, hipStream_t s, void *argp)
+{
+    void *args[] = {argp};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(kernel), dim3(NXCD * WG_PER_XCD), dim3(XT), args,
+                                      0u, s);
+}
+
+int g_xcd_disabled = 0;
+
+}  // namespace
+
+bool xcd_path_ok(DType t, const RecShape &sh, int num_cus)
+{
+    if (g_xcd_disabled || t != DType::BF16 || sh.Hp != 0 || num_cus != NXCD * WG_PER_XCD) return false;
+    if (sh.H != 256 && sh.H != 512 && sh.H != 1024) return false;
+    const int RX = (sh.B + NXCD - 1) / NXCD;
+    return RX <= 64;
+}
+
+void xcd_path_disable() { g_xcd_disabled = 1; }
+
+hipError_t xcd_tripped_read_and_clear(unsigned *tripped)
+{
+    unsigned v = 0;
+    hipError_t e = hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_xcd_tripped), sizeof(v), 0, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    *tripped = v;
+    if (v) {
+        const unsigned zero = 0;
+        e = hipMemcpyToSymbol(HIP_SYMBOL(g_xcd_tripped), &zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+    }
+    return e;
+}
+
+namespace {
+int mbx_for(int B)
+{
+    const int RX = (B + NXCD - 1) / NXCD;
+    const int m = (RX + 15) / 16;
+    return m <= 1 ? 1 : (m <= 2 ? 2 : 4);
+}
+}  // namespace
+
+hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned long long timeout, hipStream_t s)
+{
+    XFwdArgs a;
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.reverse = sh.reverse; a.RX = (sh.B + NXCD - 1) / NXCD; a.ldy = sh.ldy;
+    a.R = static_cast<const bf16_t *>(bf.R);
+    a.h0 = static_cast<const bf16_t *>(bf.h0);
+    a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
+    a.y = static_cast<bf16_t *>(bf.y);
+    a.hT = static_cast<bf16_t *>(bf.hT);
+    a.cT = bf.cT;
+    a.flags = bf.sync + XCD_FLAGS;
+    a.timeout = timeout;
+    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
+                 (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0);
+    const int m = mbx_for(sh.B);
+#define FWD_CASE(HN_, M_) \
+    if (sh.H == 32 * HN_ && m == M_) return coop512(lstm_fwd_xcd<HN_, M_>, s, &a);
+    FWD_CASE(8, 1) FWD_CASE(8, 2) FWD_CASE(8, 4)
+    FWD_CASE(16, 1) FWD_CASE(16, 2) FWD_CASE(16, 4)
+    FWD_CASE(32, 1) FWD_CASE(32, 2) FWD_CASE(32, 4)
+#undef FWD_CASE
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned long long timeout, hipStream_t s)
+{
+    XBwdArgs a;
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.reverse = sh.reverse; a.RX = (sh.B + NXCD - 1) / NXCD; a.ldy = sh.ldy;
+    a.Rt = static_cast<const bf16_t *>(bf.Rt);
+    a.dy = static_cast<const bf16_t *>(bf.dy);
+    a.dhT = static_cast<const bf16_t *>(bf.dhT);
+    a.dcT = bf.dcT; a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
+    a.dz = static_cast<bf16_t *>(bf.dz);
+    a.dh0 = static_cast<bf16_t *>(bf.dh0);
+    a.dc0 = bf.dc0;
+    a.flags = bf.sync + XCD_FLAGS;
+    a.timeout = timeout;
+    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
+                 (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 10.0 + G4 * 2.0) + G4 * sh.H * 2.0);
+    const int m = mbx_for(sh.B);
+#define BWD_CASE(HN_, M_) \
+    if (sh.H == 32 * HN_ && m == M_) return coop512(lstm_bwd_xcd<HN_, M_>, s, &a);
+    BWD_CASE(8, 1) BWD_CASE(8, 2) BWD_CASE(8, 4)
+    BWD_CASE(16, 1) BWD_CASE(16, 2) BWD_CASE(16, 4)
+    BWD_CASE(32, 1) BWD_CASE(32, 2) BWD_CASE(32, 4)
+#undef BWD_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace lstm355

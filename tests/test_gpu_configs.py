@@ -1,0 +1,58 @@
+"""Parity at the full benchmark shapes, in the launch configuration the
+benchmark times.
+
+The oracle cannot run a whole full-size step in test time, so the GPU runs
+the full mini-batch with the upstream gradient kept only on a few sampled
+batch rows (zero elsewhere).  Batch rows are independent in the LSTM, so
+  - outputs and input gradients of the sampled rows equal the oracle's on
+    those rows alone, and
+  - every weight gradient equals the oracle's weight gradient over the
+    sampled rows alone (the other rows contribute exactly zero).
+Tolerances: bf16 mode, 2e-2 on outputs, 5e-2 on gradients (normwise)."""
+import numpy as np
+import pytest
+
+import synth
+from _gpu_helpers import announce, compare, run_oracle, run_stack_gpu
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def run_masked(wl: synth.Workload, nrows=3):
+    rows = synth.sample_rows(wl.B, nrows, wl.seed)
+    mask = np.zeros(wl.B, dtype=bool)
+    mask[rows] = True
+    announce(f"{wl.name} T{wl.T} B{wl.B} layers={len(wl.layers)} rows={rows.tolist()}")
+    prob = synth.draw(wl, row_mask=mask)
+    gpu, stack = run_stack_gpu(prob)
+    announce(f"{wl.name}: gpu done, tiling={stack.dirs[0][0].tiling()}")
+    ref = run_oracle(prob, rows=rows)
+    compare(gpu, ref, wl.dtype, rows=rows, label=wl.name)
+    # rows outside the sample received no gradient at all
+    others = np.setdiff1d(np.arange(wl.B), rows)
+    assert np.all(gpu["dx"][:, others] == 0.0)
+
+
+def test_gnmt4_B128():
+    run_masked(synth.gnmt4())
+
+
+@pytest.mark.parametrize("B", synth.SWEEP_BATCHES)
+def test_gnmt4_batch_sweep(B):
+    run_masked(synth.sweep(B))
+
+
+def test_biglstm_lstmp():
+    run_masked(synth.biglstm())
+
+
+def test_gnmt8_bidirectional_residual():
+    run_masked(synth.gnmt8())

@@ -115,7 +115,15 @@ LAYER_CASES = [
     (6, 33, 48, 136, 40, "bf16", True),    # LSTMP reverse, ragged
     (3, 130, 64, 96, 0, "bf16", False),    # more batch tiles than one workgroup row
     (1, 3, 16, 16, 0, "f32", False),       # a single step
+    # XCD-local kernels (bf16, H in {256, 512, 1024}): ragged rows per XCD
+    (6, 40, 64, 256, 0, "bf16", False),    # 5 rows per XCD
+    (4, 130, 32, 512, 0, "bf16", True),    # 17 rows per XCD: two row blocks, reverse
+    (3, 500, 40, 256, 0, "bf16", False),   # 63 rows per XCD: four row blocks
+    (5, 16, 48, 1024, 0, "bf16", False),   # 2 rows per XCD, full-width cells
+    (1, 9, 16, 256, 0, "bf16", True),      # a single step
 ]
+
+XCD_VARIANT = 1000
 
 
 @pytest.mark.parametrize("T,B,I,H,Hp,dtype,reverse", LAYER_CASES)
@@ -126,6 +134,9 @@ def test_layer_parity(T, B, I, H, Hp, dtype, reverse):
     gpu = run_layer_gpu(c, T, B, I, H, Hp, dtype, reverse)
     ref = oracle_layer(c, Hp, reverse)
     check_layer(gpu, ref, dtype, label)
+    xcd = dtype == "bf16" and Hp == 0 and H in (256, 512, 1024) and (B + 7) // 8 <= 64
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
 def test_layer_without_initial_state_or_final_grads():
