@@ -22,7 +22,8 @@ struct lstm_handle {
     // reserve layout (bytes)
     size_t r_gates, r_cs, r_ms, r_total;
     // workspace layout (bytes)
-    size_t w_sync, w_dz, w_rt, w_pt, w_dH, w_dcn, w_dhn, w_part, w_total;
+    size_t w_sync, w_dz, w_rt, w_pt, w_dH, w_dcn, w_dhn, w_part, w_split, w_total;
+    size_t split_floats;
     // per-device tiling
     int dev;
     int num_cus;
@@ -143,6 +144,13 @@ extern "C" lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out
         h->w_dcn = o;  o = align256(o + (size_t)d.B * d.H * 4);
         h->w_dhn = o;  o = align256(o + (size_t)d.B * d.H * 4);
         h->w_part = o; o = align256(o + colsum_partial_floats((int)TB, (int)G4) * 4);
+        // split-K partials of the weight-gradient products (up to 4 splits)
+        {
+            size_t mn = (size_t)G4 * (size_t)(d.I > Hr ? d.I : Hr);
+            if (d.Hp && (size_t)d.Hp * d.H > mn) mn = (size_t)d.Hp * d.H;
+            h->split_floats = 4 * mn;
+        }
+        h->w_split = o; o = align256(o + h->split_floats * 4);
         h->w_total = o;
         h->dev = -1;
         h->fwd_ok = h->bwd_ok = false;
@@ -248,6 +256,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         void *Rt = wv + h->w_rt;
         void *Pt = Hp ? wv + h->w_pt : nullptr;
         void *dH = Hp ? wv + h->w_dH : nullptr;
+        float *split_ws = reinterpret_cast<float *>(wv + h->w_split);
 
         TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s));
         if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
@@ -279,6 +288,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
             g.M = (int)G4; g.N = I; g.K = (int)TB;
             g.A = dz; g.lda = G4; g.B = x; g.ldb = h->ldx; g.C = dW; g.ldc = I; g.beta = accumulate;
+            g.splitk_ws = split_ws; g.splitk_ws_floats = h->split_floats;
             TRY_HIP("dW", gemm(g, s, K_GEMM_DW));
         }
         {  // dR = sum_t dz_t^T h_{t-1}: steps after the first see y of the previous step, the first sees h0
@@ -297,6 +307,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
                     g.B = yc + (size_t)B * h->ldy * es;         // y  at t = 1 .. T-1
                 }
                 g.lda = G4; g.ldb = h->ldy; g.C = dR; g.ldc = Hr; g.beta = beta;
+                g.splitk_ws = split_ws; g.splitk_ws_floats = h->split_floats;
                 TRY_HIP("dR", gemm(g, s, K_GEMM_DR));
                 beta = 1;
             }
@@ -318,6 +329,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
             g.M = Hp; g.N = H; g.K = (int)TB;
             g.A = dH; g.lda = Hp; g.B = rv + h->r_ms; g.ldb = H; g.C = dP; g.ldc = H; g.beta = accumulate;
+            g.splitk_ws = split_ws; g.splitk_ws_floats = h->split_floats;
             TRY_HIP("dP", gemm(g, s, K_GEMM_DP));
         }
         return LSTM_OK;

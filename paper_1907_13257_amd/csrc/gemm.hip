@@ -3,22 +3,28 @@
 // the gradients dX = dZ W, dW = dZ^T X, dR = dZ^T H_prev, dP = dH^T M.
 //
 // One kernel template covers all of them.  A workgroup (4 waves, 2x2) owns a
-// BM x BN tile of C and walks K in stages of 64 bytes per row.  Both operands
-// are staged in LDS with k contiguous in every row, so the fragment reads
-// are 16-byte ds_reads for either element type.  An operand whose k is not the
-// contiguous dimension in memory (the transposed operands of the weight
-// gradients) is loaded with 16-byte global reads along m and transposed in
-// registers before the LDS write.  Two LDS stages: the global loads of stage
-// s+1 are in flight while stage s feeds the MFMAs.
+// BM x BN tile of C (up to 256x256: 128x128 per wave, accumulators in AGPRs)
+// and walks K in stages of KB bytes per row.  Both operands are staged in LDS
+// with k contiguous in every row, so every fragment read is a 16-byte
+// ds_read.  An operand whose k is not the contiguous dimension in memory (the
+// transposed operands of the weight gradients) is loaded with 16-byte global
+// reads along m and transposed in registers before the LDS write.  Two LDS
+// stages: the global loads of stage s+1 are in flight while stage s feeds
+// v_mfma_f32_32x32x16_bf16 (fp32 inputs: v_mfma_f32_32x32x2f32).
+//
+// Small outputs (the weight gradients are 4H x I at most, K = T*B long) can
+// be split along K over several workgroups; every split writes an fp32
+// partial tile and a second kernel sums the splits in a fixed order, so the
+// result does not depend on scheduling.
 #include "device_common.hpp"
 #include "kernels.hpp"
+
+#include <cstdlib>
+#include <cstring>
 
 namespace lstm355 {
 
 namespace {
-
-constexpr int KB = 64;            // bytes of k per stage and row
-constexpr int PITCH = KB + 16;    // LDS row pitch (16 B of padding against bank conflicts)
 
 struct GemmArgs {
     int M, N, K;
@@ -28,40 +34,44 @@ struct GemmArgs {
     const float *bias;
     int beta;
     int tiles_n, ntiles, per_xcd;
+    int kchunk;                  // K per split (multiple of the stage depth)
+    float *partial;              // split > 1: fp32 partials [split][M][N]
 };
 
-// Loads `NC` 16-byte vectors of one operand stage into registers.
-//   KMAJ:  chunk c = tid + i*256: row = c / 4, k-vector = c % 4.
-//   !KMAJ: thread owns one m-vector (E rows) and NC consecutive k rows.
-template <typename TI, int ROWS, bool KMAJ>
-struct OperandLoader {
+// Global -> register -> LDS staging of one operand for one K stage.
+//   KMAJ:  16-byte vector c = tid + i*256 is row c / VPR, k-vector c % VPR.
+//   !KMAJ: thread owns one m-vector (E rows) and NC consecutive k rows, and
+//          transposes them in registers (element e of vector i is
+//          operand(m = mv*E + e, k = kg*NC + i)).
+template <typename TI, int ROWS, bool KMAJ, int KB>
+struct Loader {
     static constexpr int E = 16 / (int)sizeof(TI);
-    static constexpr int KS = KB / (int)sizeof(TI);         // k per stage
-    static constexpr int NC = ROWS / 64;                    // vectors per thread
+    static constexpr int KS = KB / (int)sizeof(TI);   // k per stage
+    static constexpr int VPR = KB / 16;               // vectors per row per stage
+    static constexpr int NC = ROWS * VPR / 256;       // vectors per thread
+    static constexpr int PITCH = KB + 16;
+    static constexpr int MV = ROWS / E;
     u32x4 v[NC];
 
-    __device__ __forceinline__ void load(const char *base, long ld, int r0, int rows_total, int k0, int K, int tid)
+    __device__ __forceinline__ void load(const char *base, long ld, int r0, int rows_total, int k0, int kend, int tid)
     {
         if (KMAJ) {
 #pragma unroll
             for (int i = 0; i < NC; ++i) {
-                int c = tid + i * 256;
-                int row = c >> 2, kv = c & 3;
-                int gr = r0 + row, gk = k0 + kv * E;
-                v[i] = (gr < rows_total && gk < K)
-                           ? ldg16(base + ((long)gr * ld + gk) * (long)sizeof(TI))
-                           : zero16();
+                const int c = tid + i * 256;
+                const int row = c / VPR, kv = c % VPR;
+                const int gr = r0 + row, gk = k0 + kv * E;
+                v[i] = (gr < rows_total && gk < kend) ? ldg16(base + ((long)gr * ld + gk) * (long)sizeof(TI))
+                                                      : zero16();
             }
         } else {
-            constexpr int MV = ROWS / E;                 // m-vectors per stage
-            int mv = tid % MV, kg = tid / MV;
-            int gm = r0 + mv * E;
+            const int mv = tid % MV, kg = tid / MV;
+            const int gm = r0 + mv * E;
 #pragma unroll
             for (int i = 0; i < NC; ++i) {
-                int gk = k0 + kg * NC + i;
-                v[i] = (gm < rows_total && gk < K)
-                           ? ldg16(base + ((long)gk * ld + gm) * (long)sizeof(TI))
-                           : zero16();
+                const int gk = k0 + kg * NC + i;
+                v[i] = (gm < rows_total && gk < kend) ? ldg16(base + ((long)gk * ld + gm) * (long)sizeof(TI))
+                                                      : zero16();
             }
         }
     }
@@ -71,19 +81,17 @@ struct OperandLoader {
         if (KMAJ) {
 #pragma unroll
             for (int i = 0; i < NC; ++i) {
-                int c = tid + i * 256;
-                int row = c >> 2, kv = c & 3;
+                const int c = tid + i * 256;
+                const int row = c / VPR, kv = c % VPR;
                 *reinterpret_cast<u32x4 *>(lds + row * PITCH + kv * 16) = v[i];
             }
         } else {
-            constexpr int MV = ROWS / E;
-            int mv = tid % MV, kg = tid / MV;
-            // element e of vector i is A(m = mv*E + e, k = kg*NC + i)
+            const int mv = tid % MV, kg = tid / MV;
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 char *dst = lds + (mv * E + e) * PITCH + kg * NC * (int)sizeof(TI);
                 if (sizeof(TI) == 2) {
-                    unsigned w[NC / 2 > 0 ? NC / 2 : 1];
+                    unsigned w[NC / 2];
 #pragma unroll
                     for (int p = 0; p < NC / 2; ++p) {
                         unsigned lo = v[2 * p][e >> 1], hi = v[2 * p + 1][e >> 1];
@@ -91,8 +99,8 @@ struct OperandLoader {
                         hi = (e & 1) ? (hi & 0xffff0000u) : (hi << 16);
                         w[p] = lo | hi;
                     }
-                    if (NC == 2) {
-                        *reinterpret_cast<unsigned *>(dst) = w[0];
+                    if (NC == 8) {
+                        *reinterpret_cast<u32x4 *>(dst) = u32x4{w[0], w[1], w[2], w[3]};
                     } else if (NC == 4) {
                         *reinterpret_cast<u32x2 *>(dst) = u32x2{w[0], w[1]};
                     } else {
@@ -100,37 +108,47 @@ struct OperandLoader {
                         for (int p = 0; p < NC / 2; ++p) reinterpret_cast<unsigned *>(dst)[p] = w[p];
                     }
                 } else {
+                    if (NC % 4 == 0) {
 #pragma unroll
-                    for (int p = 0; p < NC; ++p) reinterpret_cast<unsigned *>(dst)[p] = v[p][e];
+                        for (int p = 0; p < NC; p += 4)
+                            *reinterpret_cast<u32x4 *>(dst + p * 4) = u32x4{v[p][e], v[p + 1][e], v[p + 2][e], v[p + 3][e]};
+                    } else {
+#pragma unroll
+                        for (int p = 0; p < NC; ++p) reinterpret_cast<unsigned *>(dst)[p] = v[p][e];
+                    }
                 }
             }
         }
     }
 };
 
-template <typename TI, typename TO, int BM, int BN, bool AK, bool BKM>
-__global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g)
+template <typename TI, typename TO, int BM, int BN, int KB, bool AK, bool BKM>
+__global__ __launch_bounds__(256, (BM * BN > 128 * 128) ? 1 : 2) void gemm_kernel(GemmArgs g)
 {
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
     constexpr int KS = KB / (int)sizeof(TI);
+    constexpr int PITCH = KB + 16;
     constexpr int STAGE = (BM + BN) * PITCH;
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    constexpr int SUB = KB / 32;                      // 32-byte k substeps per stage
+    extern __shared__ __attribute__((aligned(16))) char smem[];
 
     // XCD-aware order: consecutive workgroups go to different XCDs, so give
-    // each XCD a contiguous run of tiles (shared A rows stay in its L2).
+    // each XCD a contiguous run of tiles (shared operand rows stay in its L2).
     const int bid = blockIdx.x;
     const int tile = (bid & 7) * g.per_xcd + (bid >> 3);
     if (tile >= g.ntiles) return;
     const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
+    const int kbeg = blockIdx.y * g.kchunk;
+    const int kend = min(g.K, kbeg + g.kchunk);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
 
-    OperandLoader<TI, BM, AK> la;
-    OperandLoader<TI, BN, BKM> lb;
+    Loader<TI, BM, AK, KB> la;
+    Loader<TI, BN, BKM, KB> lb;
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -140,11 +158,13 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    const int nst = (g.K + KS - 1) / KS;
-    la.load(g.A, g.lda, m0, g.M, 0, g.K, tid);
-    lb.load(g.B, g.ldb, n0, g.N, 0, g.K, tid);
-    la.store(smem, tid);
-    lb.store(smem + BM * PITCH, tid);
+    const int nst = (kend - kbeg + KS - 1) / KS;
+    if (nst > 0) {
+        la.load(g.A, g.lda, m0, g.M, kbeg, kend, tid);
+        lb.load(g.B, g.ldb, n0, g.N, kbeg, kend, tid);
+        la.store(smem, tid);
+        lb.store(smem + BM * PITCH, tid);
+    }
     __syncthreads();
 
     for (int st = 0; st < nst; ++st) {
@@ -152,11 +172,11 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g)
         const char *sb = sa + BM * PITCH;
         const bool more = st + 1 < nst;
         if (more) {
-            la.load(g.A, g.lda, m0, g.M, (st + 1) * KS, g.K, tid);
-            lb.load(g.B, g.ldb, n0, g.N, (st + 1) * KS, g.K, tid);
+            la.load(g.A, g.lda, m0, g.M, kbeg + (st + 1) * KS, kend, tid);
+            lb.load(g.B, g.ldb, n0, g.N, kbeg + (st + 1) * KS, kend, tid);
         }
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
+        for (int s = 0; s < SUB; ++s) {
             u32x4 fa[FM], fb[FN];
             const int off = s * 32 + (lane >> 5) * 16;
 #pragma unroll
@@ -179,29 +199,54 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmArgs g)
     }
 
     // epilogue: lane holds rows 8*(v/4) + 4*(lane/32) + v%4, column lane%32
+    const bool split = g.partial != nullptr;
+    float *part = split ? g.partial + (long)blockIdx.y * g.M * g.N : nullptr;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
             const int col = n0 + wn * WN + j * 32 + (lane & 31);
             if (col >= g.N) continue;
-            const float bv = g.bias ? g.bias[col] : 0.0f;
+            const float bv = (!split && g.bias) ? g.bias[col] : 0.0f;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
                 if (row < g.M) {
-                    TO *cp = reinterpret_cast<TO *>(g.C) + (long)row * g.ldc + col;
-                    float r = acc[i][j][v] + bv;
-                    if (g.beta) r += to_f32(*cp);
-                    *cp = from_f32<TO>(r);
+                    if (split) {
+                        part[(long)row * g.N + col] = acc[i][j][v];
+                    } else {
+                        TO *cp = reinterpret_cast<TO *>(g.C) + (long)row * g.ldc + col;
+                        float r = acc[i][j][v] + bv;
+                        if (g.beta) r += to_f32(*cp);
+                        *cp = from_f32<TO>(r);
+                    }
                 }
             }
         }
 }
 
-template <typename TI, typename TO, int BM, int BN, bool AK, bool BKM>
-hipError_t launch_gemm(const GemmDesc &d, hipStream_t s)
+// C[m][n] = (beta ? C : 0) + bias[n] + sum over splits of partial[s][m][n], in split order.
+template <typename TO>
+__global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ partial, int splits, int M, int N,
+                                                      const float *bias, int beta, TO *C, long ldc)
 {
+    const long total = (long)M * N;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+        const int m = (int)(i / N), n = (int)(i % N);
+        float r = 0.0f;
+        for (int s = 0; s < splits; ++s) r += partial[(long)s * total + i];
+        if (bias) r += bias[n];
+        TO *cp = C + (long)m * ldc + n;
+        if (beta) r += to_f32(*cp);
+        *cp = from_f32<TO>(r);
+    }
+}
+
+template <typename TI, typename TO, int BM, int BN, int KB, bool AK, bool BKM>
+hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
+{
+    constexpr int KS = KB / (int)sizeof(TI);
+    constexpr int LDS = 2 * (BM + BN) * (KB + 16);
     GemmArgs g;
     g.M = d.M; g.N = d.N; g.K = d.K;
     g.A = static_cast<const char *>(d.A); g.lda = d.lda;
@@ -212,20 +257,82 @@ hipError_t launch_gemm(const GemmDesc &d, hipStream_t s)
     g.tiles_n = (d.N + BN - 1) / BN;
     g.ntiles = tiles_m * g.tiles_n;
     g.per_xcd = (g.ntiles + 7) / 8;
-    const int grid = g.per_xcd * 8;
-    hipLaunchKernelGGL((gemm_kernel<TI, TO, BM, BN, AK, BKM>), dim3(grid), dim3(256), 0, s, g);
+    g.kchunk = ((d.K + splits - 1) / splits + KS - 1) / KS * KS;
+    splits = (d.K + g.kchunk - 1) / g.kchunk;
+    g.partial = splits > 1 ? d.splitk_ws : nullptr;
+    auto kern = gemm_kernel<TI, TO, BM, BN, KB, AK, BKM>;
+    if (LDS > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(256), LDS, s, g);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const long total = (long)d.M * d.N;
+    long grid = (total + 255) / 256;
+    if (grid > 4096) grid = 4096;
+    hipLaunchKernelGGL(splitk_reduce<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
+                       d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
     return hipGetLastError();
+}
+
+// Tile and split choice: a crude model of per-CU efficiency per tile shape,
+// quantised over 256 CUs, plus the traffic of the split-K partials.
+struct Choice {
+    int tile;     // 0: 256x256, 1: 256x128, 2: 128x256, 3: 128x128
+    int splits;
+};
+
+Choice choose(const GemmDesc &d, size_t es)
+{
+    static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
+    static const double eff[4] = {1.0, 0.8, 0.8, 0.55};
+    const char *env = std::getenv("LSTM355_GEMM_TILE");   // tuning override: "tile,splits"
+    if (env) {
+        int t = std::atoi(env), sp = 1;
+        const char *c = std::strchr(env, ',');
+        if (c) sp = std::atoi(c + 1);
+        if (t >= 0 && t < 4 && sp >= 1) return Choice{t, sp};
+    }
+    const int cus = 256;
+    const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
+    Choice best{3, 1};
+    double best_t = 1e30;
+    for (int t = 0; t < 4; ++t) {
+        if (es == 4 && t != 3) continue;            // fp32 inputs: the 128x128 tile only
+        const long tiles = (long)((d.M + BMs[t] - 1) / BMs[t]) * ((d.N + BNs[t] - 1) / BNs[t]);
+        for (int sp = 1; sp <= 8; sp *= 2) {
+            if (sp > 1 && (!d.splitk_ws || (size_t)sp * d.M * d.N > d.splitk_ws_floats)) break;
+            if (sp > 1 && d.K / sp < 512) break;
+            const long items = tiles * sp;
+            const long waves = (items + cus - 1) / cus;
+            const double item_t = 2.0 * BMs[t] * BNs[t] * ((double)d.K / sp) / (cu_rate * eff[t]);
+            double tt = waves * item_t;
+            if (sp > 1) tt += ((double)sp + 1.0) * d.M * d.N * 4.0 / 5.0e12;
+            if (tt < best_t * 0.97) {
+                best_t = tt;
+                best = Choice{t, sp};
+            }
+        }
+    }
+    return best;
 }
 
 template <typename TI, typename TO, bool AK, bool BKM>
 hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
 {
-    // Large outputs take 256x128 tiles; otherwise 128x128 keeps more
-    // workgroups in flight on the 256 CUs.
-    const long t256 = (long)((d.M + 255) / 256) * ((d.N + 127) / 128);
-    if (t256 >= 512)
-        return launch_gemm<TI, TO, 256, 128, AK, BKM>(d, s);
-    return launch_gemm<TI, TO, 128, 128, AK, BKM>(d, s);
+    const Choice c = choose(d, sizeof(TI));
+    if constexpr (sizeof(TI) == 4) {
+        return launch_gemm<TI, TO, 128, 128, 64, AK, BKM>(d, c.splits, s);
+    } else {
+    switch (c.tile) {
+    case 0: return launch_gemm<TI, TO, 256, 256, 128, AK, BKM>(d, c.splits, s);
+    case 1: return launch_gemm<TI, TO, 256, 128, 128, AK, BKM>(d, c.splits, s);
+    case 2: return launch_gemm<TI, TO, 128, 256, 128, AK, BKM>(d, c.splits, s);
+    default: return launch_gemm<TI, TO, 128, 128, 128, AK, BKM>(d, c.splits, s);
+    }
+    }
 }
 
 template <typename TI>

@@ -49,6 +49,8 @@ struct GemmDesc {
     void *C; long ldc;
     const float *bias;
     int beta;
+    float *splitk_ws;          // optional fp32 scratch for split-K partials
+    size_t splitk_ws_floats;
 };
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
 
