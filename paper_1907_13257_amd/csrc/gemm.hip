@@ -225,6 +225,240 @@ __global__ __launch_bounds__(256, (BM * BN > 128 * 128) ? 1 : 2) void gemm_kerne
         }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernel with direct global -> LDS loads (no register staging).
+//
+// Operands reach LDS through bounds-checked buffer loads that write LDS
+// directly (16 bytes per lane; a wave fills 1 KiB per instruction).  Rows
+// past the end of a K-major operand read as zero.  A ring of NS stages of KD
+// k (KD = 32 or 64) keeps NS-1 stages of loads in flight while one is
+// consumed.  LDS rows are XOR-swizzled in 16-byte chunks so that the lanes
+// one LDS cycle serves (a 256-byte window of 64 four-byte banks) touch
+// distinct chunk positions:
+//   K-major tile [rows][2 KD bytes]: chunk c of row r lives at slot
+//     c ^ ((r / RW) % CH), RW = 256 / (2 KD) rows per window, CH chunks per row;
+//   M-major tile [KD k][rows]: chunk c of k-row k lives at slot c ^ (4 (k & 3)),
+//     so the four k-rows read by 32 lanes of ds_read_b64_tr_b16 fall in
+//     disjoint 64-byte ranges.
+// M-major operands (the transposed operands of dW, dR, dP, dX) are read with
+// ds_read_b64_tr_b16: in each group of 16 lanes, output lane i, element e is
+// element (i % 4) of the 8 bytes addressed by source lane 4e + i/4, so source
+// lanes addressing (k = kb + s/4, m = mb + 4 (s % 4)) deliver to lane i the
+// four k values kb..kb+3 of column m = mb + i.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned lds_addr(const char *p) { return (unsigned)(uintptr_t)p; }
+
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt not waited on (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void waitcnt_vm()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | (0x7 << 4) | (0xf << 8) | ((N >> 4) << 14));
+}
+
+// Buffer -> LDS load of 16 bytes per lane into LDS bytes [lds, lds + 1 KiB).
+// Issued as inline asm so the compiler does not see an LDS write it must wait
+// for before every LDS read; the kernel orders these loads itself with
+// s_waitcnt vmcnt(N) and s_barrier.
+__device__ __forceinline__ void dma16(u32x4 rsrc, unsigned lds_byte, unsigned voff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_byte), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+
+template <int ROWS, bool KMAJ, int KD>
+struct DlLayout {
+    static constexpr int RB = KD * 2;             // K-major: bytes per row per stage
+    static constexpr int CH = RB / 16;            // K-major: chunks per row
+    static constexpr int RW = 256 / RB;           // K-major: rows per 256-byte window
+    static constexpr int RP = ROWS * 2;           // M-major: bytes per k-row
+    static constexpr int BYTES = ROWS * RB;       // either layout
+    static constexpr int NI = BYTES / 1024 / 4;   // 1 KiB instructions per wave per stage
+
+    __device__ static __forceinline__ int kslot(int row, int c) { return c ^ ((row / RW) % CH); }
+    __device__ static __forceinline__ int mslot(int k, int c) { return c ^ (4 * (k & 3)); }
+};
+
+// One operand of one stage: ROWS rows, KD k.
+template <int ROWS, bool KMAJ, int KD>
+struct DmaOperand {
+    using L = DlLayout<ROWS, KMAJ, KD>;
+    u32x4 rsrc;                                   // buffer descriptor (base, limit, format)
+    long ld;                                      // elements
+    int r0;
+
+    __device__ __forceinline__ void init(const char *base, long ld_, int r0_, long bound_bytes)
+    {
+        const unsigned nrec = bound_bytes > 0x7fffffffL ? 0x7fffffffu : (unsigned)bound_bytes;
+        const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+        rsrc = u32x4{(unsigned)b, (unsigned)(b >> 32) & 0xffffu, nrec, 0x00020000u};
+        ld = ld_;
+        r0 = r0_;
+    }
+
+    __device__ __forceinline__ void issue(unsigned dst, int k0, int wave, int lane) const
+    {
+#pragma unroll
+        for (int i = 0; i < L::NI; ++i) {
+            const int q = wave * L::NI + i;
+            const int byte = q * 1024 + lane * 16;
+            unsigned off;
+            if (KMAJ) {
+                const int row = byte / L::RB, p = (byte % L::RB) >> 4;
+                const int c = L::kslot(row, p);   // the swizzle is an involution
+                off = (unsigned)((((long)(r0 + row) * ld + k0) << 1) + c * 16);
+            } else {
+                const int k = byte / L::RP, p = (byte % L::RP) >> 4;
+                const int c = L::mslot(k, p);
+                off = (unsigned)((((long)(k0 + k) * ld + r0) << 1) + c * 16);
+            }
+            dma16(rsrc, __builtin_amdgcn_readfirstlane(dst + q * 1024), off);
+        }
+    }
+};
+
+// Byte offset (within a stage's operand region) of this lane's fragment read
+// for k substep s (16 k): K-major one b128; M-major two b64 transpose reads.
+template <int ROWS, bool KMAJ, int KD>
+__device__ __forceinline__ unsigned frag_off(int rowbase, int s, int r, int lane)
+{
+    using L = DlLayout<ROWS, KMAJ, KD>;
+    if (KMAJ) {
+        const int row = rowbase + (lane & 31);
+        const int c = 2 * s + (lane >> 5);
+        return (unsigned)(row * L::RB + (L::kslot(row, c) << 4));
+    } else {
+        const int gq = lane >> 4, sl = lane & 15;
+        const int k = 16 * s + (gq >> 1) * 8 + 4 * r + (sl >> 2);
+        const int m = rowbase + 16 * (gq & 1) + 4 * (sl & 3);
+        const int c = m >> 3;
+        return (unsigned)(k * L::RP + (L::mslot(k, c) << 4) + ((m & 7) << 1));
+    }
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4_t;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+template <int F, int ROWS, bool KMAJ, int KD>
+__device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int rowbase0, int s, int lane)
+{
+#pragma unroll
+    for (int i = 0; i < F; ++i) {
+        if (KMAJ) {
+            f[i] = *(const lds_u32x4_t *)(base + frag_off<ROWS, true, KD>(rowbase0 + i * 32, s, 0, lane));
+        } else {
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4_t *)(base + frag_off<ROWS, false, KD>(rowbase0 + i * 32, s, 0, lane)));
+            const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4_t *)(base + frag_off<ROWS, false, KD>(rowbase0 + i * 32, s, 1, lane)));
+            const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+            f[i] = u32x4{l2[0], l2[1], h2[0], h2[1]};
+        }
+    }
+}
+
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS>
+__global__ __launch_bounds__(256, 1) void gemm_dl_kernel(GemmArgs g)
+{
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int FM = WM / 32, FN = WN / 32;
+    using LA = DlLayout<BM, AK, KD>;
+    using LB = DlLayout<BN, BKM, KD>;
+    constexpr int ABYTES = LA::BYTES, STAGE = LA::BYTES + LB::BYTES;
+    constexpr int LPW = LA::NI + LB::NI;          // DMA instructions per wave per stage
+    extern __shared__ __attribute__((aligned(1024))) char smem[];
+
+    const int bid = blockIdx.x;
+    const int tile = (bid & 7) * g.per_xcd + (bid >> 3);
+    if (tile >= g.ntiles) return;
+    const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kbeg = blockIdx.y * g.kchunk;
+    const int kend = min(g.K, kbeg + g.kchunk);
+    const int nst = (kend - kbeg) / KD;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+
+    DmaOperand<BM, AK, KD> da;
+    DmaOperand<BN, BKM, KD> db;
+    da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)g.K * g.lda * 2);
+    db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const unsigned sbase = lds_addr(smem);
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nst) {
+            const unsigned st_base = sbase + s * STAGE;
+            da.issue(st_base, kbeg + s * KD, wave, lane);
+            db.issue(st_base + ABYTES, kbeg + s * KD, wave, lane);
+        }
+
+    for (int st = 0; st < nst; ++st) {
+        // stage st has landed once at most the later stages' loads are outstanding
+        if (st + NS - 2 < nst)
+            waitcnt_vm<(NS - 2) * LPW>();
+        else
+            waitcnt_vm<0>();
+        asm volatile("s_barrier" ::: "memory");
+        if (st + NS - 1 < nst) {
+            const unsigned st_base = sbase + ((st + NS - 1) % NS) * STAGE;
+            da.issue(st_base, kbeg + (st + NS - 1) * KD, wave, lane);
+            db.issue(st_base + ABYTES, kbeg + (st + NS - 1) * KD, wave, lane);
+        }
+        const char *abase = smem + (st % NS) * STAGE;
+        const char *bbase = abase + ABYTES;
+#pragma unroll
+        for (int s = 0; s < KD / 16; ++s) {
+            u32x4 fa[FM], fb[FN];
+            read_frags<FM, BM, AK, KD>(fa, abase, wm * WM, s, lane);
+            read_frags<FN, BN, BKM, KD>(fb, bbase, wn * WN, s, lane);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) mfma32(acc[i][j], fa[i], fb[j], bf16_t{});
+        }
+    }
+
+    const bool split = g.partial != nullptr;
+    float *part = split ? g.partial + (long)blockIdx.y * g.M * g.N : nullptr;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int col = n0 + wn * WN + j * 32 + (lane & 31);
+            if (col >= g.N) continue;
+            const float bv = (!split && g.bias) ? g.bias[col] : 0.0f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                if (row < g.M) {
+                    if (split) {
+                        part[(long)row * g.N + col] = acc[i][j][v];
+                    } else {
+                        TO *cp = reinterpret_cast<TO *>(g.C) + (long)row * g.ldc + col;
+                        float r = acc[i][j][v] + bv;
+                        if (g.beta) r += to_f32(*cp);
+                        *cp = from_f32<TO>(r);
+                    }
+                }
+            }
+        }
+}
+
 // C[m][n] = (beta ? C : 0) + bias[n] + sum over splits of partial[s][m][n], in split order.
 template <typename TO>
 __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ partial, int splits, int M, int N,
@@ -240,6 +474,38 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ p
         if (beta) r += to_f32(*cp);
         *cp = from_f32<TO>(r);
     }
+}
+
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS>
+hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
+{
+    constexpr int LDS = NS * (BM + BN) * KD * 2;
+    GemmArgs g;
+    g.M = d.M; g.N = d.N; g.K = d.K;
+    g.A = static_cast<const char *>(d.A); g.lda = d.lda;
+    g.B = static_cast<const char *>(d.B); g.ldb = d.ldb;
+    g.C = static_cast<char *>(d.C); g.ldc = d.ldc;
+    g.bias = d.bias; g.beta = d.beta;
+    const int tiles_m = (d.M + BM - 1) / BM;
+    g.tiles_n = (d.N + BN - 1) / BN;
+    g.ntiles = tiles_m * g.tiles_n;
+    g.per_xcd = (g.ntiles + 7) / 8;
+    g.kchunk = ((d.K + splits - 1) / splits + KD - 1) / KD * KD;
+    splits = (d.K + g.kchunk - 1) / g.kchunk;
+    g.partial = splits > 1 ? d.splitk_ws : nullptr;
+    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(256), LDS, s, g);
+    e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const long total = (long)d.M * d.N;
+    long grid = (total + 255) / 256;
+    if (grid > 4096) grid = 4096;
+    hipLaunchKernelGGL(splitk_reduce<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
+                       d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
+    return hipGetLastError();
 }
 
 template <typename TI, typename TO, int BM, int BN, int KB, bool AK, bool BKM>
@@ -284,6 +550,8 @@ struct Choice {
     int splits;
 };
 
+bool dl_ok(const GemmDesc &d, int BM, int BN, int splits);
+
 Choice choose(const GemmDesc &d, size_t es)
 {
     static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
@@ -295,8 +563,28 @@ Choice choose(const GemmDesc &d, size_t es)
         if (c) sp = std::atoi(c + 1);
         if (t >= 0 && t < 4 && sp >= 1) return Choice{t, sp};
     }
-    const int cus = 256;
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
+    if (es == 2 && dl_ok(d, 128, 128, 1)) {
+        // direct-to-LDS 128x128 tiles run two workgroups per CU (512 slots);
+        // split K only to fill the slots
+        Choice best{3, 1};
+        double best_t = 1e30;
+        const long tiles = (long)((d.M + 127) / 128) * ((d.N + 127) / 128);
+        for (int sp = 1; sp <= 8; sp *= 2) {
+            if (sp > 1 && (!d.splitk_ws || (size_t)sp * d.M * d.N > d.splitk_ws_floats)) break;
+            if (sp > 1 && d.K / sp < 512) break;
+            const long items = tiles * sp;
+            const long waves = (items + 511) / 512;
+            double tt = waves * 2.0 * 128 * 128 * ((double)d.K / sp) / (cu_rate * 0.5);
+            if (sp > 1) tt += ((double)sp + 1.0) * d.M * d.N * 4.0 / 5.0e12;
+            if (tt < best_t * 0.97) {
+                best_t = tt;
+                best = Choice{3, sp};
+            }
+        }
+        return best;
+    }
+    const int cus = 256;
     Choice best{3, 1};
     double best_t = 1e30;
     for (int t = 0; t < 4; ++t) {
@@ -319,6 +607,22 @@ Choice choose(const GemmDesc &d, size_t es)
     return best;
 }
 
+// The direct-to-LDS kernel needs whole 32-deep K stages and, for an operand
+// whose rows are the contiguous dimension in memory, whole tiles of rows.
+bool dl_ok(const GemmDesc &d, int BM, int BN, int splits)
+{
+    const char *env = std::getenv("LSTM355_GEMM_DL");
+    if (env && env[0] == '0') return false;
+    if (d.K % 32) return false;
+    if (!d.a_kmajor && d.M % BM) return false;
+    if (!d.b_kmajor && d.N % BN) return false;
+    const long ea = d.a_kmajor ? (long)d.M * d.lda : (long)d.K * d.lda;
+    const long eb = d.b_kmajor ? (long)d.N * d.ldb : (long)d.K * d.ldb;
+    if (ea * 2 > 0x7fffffffL || eb * 2 > 0x7fffffffL) return false;
+    (void)splits;
+    return true;
+}
+
 template <typename TI, typename TO, bool AK, bool BKM>
 hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
 {
@@ -326,12 +630,31 @@ hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
     if constexpr (sizeof(TI) == 4) {
         return launch_gemm<TI, TO, 128, 128, 64, AK, BKM>(d, c.splits, s);
     } else {
-    switch (c.tile) {
-    case 0: return launch_gemm<TI, TO, 256, 256, 128, AK, BKM>(d, c.splits, s);
-    case 1: return launch_gemm<TI, TO, 256, 128, 128, AK, BKM>(d, c.splits, s);
-    case 2: return launch_gemm<TI, TO, 128, 256, 128, AK, BKM>(d, c.splits, s);
-    default: return launch_gemm<TI, TO, 128, 128, 128, AK, BKM>(d, c.splits, s);
-    }
+        static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
+        if (dl_ok(d, BMs[c.tile], BNs[c.tile], c.splits)) {
+            const char *kd = std::getenv("LSTM355_GEMM_KD");
+            const bool deep = kd ? std::atoi(kd) == 64 : false;
+            if (deep && d.K % 64 == 0) {
+                switch (c.tile) {
+                case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 3>(d, c.splits, s);
+                case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 3>(d, c.splits, s);
+                case 3: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4>(d, c.splits, s);
+                default: break;
+                }
+            }
+            switch (c.tile) {
+            case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4>(d, c.splits, s);
+            case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 4>(d, c.splits, s);
+            case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 4>(d, c.splits, s);
+            default: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4>(d, c.splits, s);
+            }
+        }
+        switch (c.tile) {
+        case 0: return launch_gemm<TI, TO, 256, 256, 128, AK, BKM>(d, c.splits, s);
+        case 1: return launch_gemm<TI, TO, 256, 128, 128, AK, BKM>(d, c.splits, s);
+        case 2: return launch_gemm<TI, TO, 128, 256, 128, AK, BKM>(d, c.splits, s);
+        default: return launch_gemm<TI, TO, 128, 128, 128, AK, BKM>(d, c.splits, s);
+        }
     }
 }
 
