@@ -143,7 +143,11 @@ extern "C" lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out
         h->w_dH = o;   o = align256(o + (d.Hp ? (size_t)TB * d.Hp * h->es : 0));
         h->w_dcn = o;  o = align256(o + (size_t)d.B * d.H * 4);
         h->w_dhn = o;  o = align256(o + (size_t)d.B * d.H * 4);
-        h->w_part = o; o = align256(o + colsum_partial_floats((int)TB, (int)G4) * 4);
+        {
+            size_t pf = colsum_partial_floats((int)TB, (int)G4);
+            if (pf < (size_t)8 * G4) pf = (size_t)8 * G4;   // per-XCD bias partials
+            h->w_part = o; o = align256(o + pf * 4);
+        }
         // split-K partials of the weight-gradient products (up to 4 splits)
         {
             size_t mn = (size_t)G4 * (size_t)(d.I > Hr ? d.I : Hr);
@@ -270,8 +274,10 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         bb.dcn = reinterpret_cast<float *>(wv + h->w_dcn);
         bb.dhn = reinterpret_cast<float *>(wv + h->w_dhn);
         bb.dh0 = dh0; bb.dc0 = dc0;
+        bb.dbpart = reinterpret_cast<float *>(wv + h->w_part);
         bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        if (xcd_path_ok(h->dt, sh, h->num_cus))
+        const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+        if (xcd)
             TRY_HIP("backward recurrence (XCD-local)", launch_backward_xcd(sh, bb, watchdog_ticks(), s));
         else
             TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
@@ -323,7 +329,10 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             }
             if (!beta) TRY_HIP("dR zero", fill_u32(dR, (size_t)G4 * Hr, 0u, s));
         }
-        TRY_HIP("db", colsum(h->dt, dz, (int)TB, (int)G4, reinterpret_cast<float *>(wv + h->w_part), db, accumulate, s));
+        if (xcd)   // the recurrence left one fp32 partial per XCD
+            TRY_HIP("db", sum_rows(reinterpret_cast<const float *>(wv + h->w_part), 8, (int)G4, db, accumulate, s));
+        else
+            TRY_HIP("db", colsum(h->dt, dz, (int)TB, (int)G4, reinterpret_cast<float *>(wv + h->w_part), db, accumulate, s));
         if (Hp) {  // dP = sum_t dh_t^T m_t
             GemmDesc g{};
             g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;

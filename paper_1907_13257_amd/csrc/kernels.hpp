@@ -60,6 +60,8 @@ hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
 // dst[c] (+)= sum_r src[r][c] over a [rows][cols] matrix of element type t, in fp32, deterministic;
 // `partial` holds colsum_partial_floats(rows, cols) floats of scratch.
 size_t colsum_partial_floats(int rows, int cols);
+// dst[c] (+)= sum_{r < rows} src[r][c] for fp32 partial rows, in row order.
+hipError_t sum_rows(const float *src, int rows, int cols, float *dst, int accumulate, hipStream_t s);
 hipError_t colsum(DType t, const void *src, int rows, int cols, float *partial, float *dst, int accumulate, hipStream_t s);
 hipError_t add(DType t, size_t n, const void *a, const void *b, void *out, hipStream_t s);
 
@@ -110,6 +112,7 @@ struct BwdBufs {
     float *dhn;         // [B][H] carry of dh between steps (plain LSTM)
     void *dh0;
     float *dc0;
+    float *dbpart;      // XCD-local kernel: [8][4H] per-XCD partial bias gradients
     unsigned *sync;
 };
 hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, const BwdBufs &b, hipStream_t s);

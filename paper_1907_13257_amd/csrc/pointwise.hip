@@ -105,6 +105,13 @@ hipError_t colsum(DType t, const void *src, int rows, int cols, float *partial, 
     return hipGetLastError();
 }
 
+hipError_t sum_rows(const float *src, int rows, int cols, float *dst, int accumulate, hipStream_t s)
+{
+    ProfScope ps(K_SMALL, s, 0.0, (double)rows * cols * 4.0);
+    hipLaunchKernelGGL(colsum_pass2, dim3((cols + 255) / 256), dim3(256), 0, s, src, rows, cols, dst, accumulate);
+    return hipGetLastError();
+}
+
 hipError_t add(DType t, size_t n, const void *a, const void *b, void *out, hipStream_t s)
 {
     ProfScope ps(K_SMALL, s, 0.0, 3.0 * n * dsize(t));

@@ -211,22 +211,31 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                 const float c = fg * creg[mb] + ig * gg;
                 const float m = og * tanh_f(c);
                 creg[mb] = c;
-                float *gp = a.gates + ((long)t * B + b) * G4 + cj;
-                gp[0] = ig;
-                gp[H] = fg;
-                gp[2 * H] = gg;
-                gp[3 * H] = og;
-                a.cs[((long)t * B + b) * H + cj] = c;
+                // the saved activations are stored after the step flag is published
+                gx[mb][0] = ig;
+                gx[mb][1] = fg;
+                gx[mb][2] = gg;
+                gx[mb][3] = og;
                 const bf16_t hv = f32_to_bf16(m);
                 a.y[((long)t * B + b) * a.ldy + cj] = hv;
-                if (last) {
-                    if (a.hT) a.hT[(long)b * H + cj] = hv;
-                    if (a.cT) a.cT[(long)b * H + cj] = c;
-                }
+                if (last && a.hT) a.hT[(long)b * H + cj] = hv;
             }
             __syncthreads();
         }
         if (!last) publish(a.flags, xcd * WG_PER_XCD + slot, (unsigned)(s + 1));
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + cr;
+            if (has_cell && b < rowend) {
+                float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+                gp[0] = gx[mb][0];
+                gp[H] = gx[mb][1];
+                gp[2 * H] = gx[mb][2];
+                gp[3 * H] = gx[mb][3];
+                a.cs[((long)t * B + b) * H + cj] = creg[mb];
+                if (last && a.cT) a.cT[(long)b * H + cj] = creg[mb];
+            }
+        }
         tprev = t;
     }
 }
@@ -238,6 +247,7 @@ struct XBwdArgs {
     const float *dcT, *c0, *gates, *cs;
     bf16_t *dz, *dh0;
     float *dc0;
+    float *dbpart;          // [8][4H]: per-XCD sums over its rows and all steps of dz
     unsigned *flags;
     unsigned long long timeout;
 };
@@ -276,6 +286,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
     float dhn[MBX], dcn[MBX];
+    float dbacc[4] = {0.f, 0.f, 0.f, 0.f};   // this thread's rows, summed over steps
 #pragma unroll
     for (int mb = 0; mb < MBX; ++mb) {
         const int b = row0 + mb * 16 + cr;
@@ -312,11 +323,17 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
                 const float d_o = dm * tc;
                 const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
                 const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv[mb];
+                const float zi = d_i * ig * (1.0f - ig), zf = d_f * fg * (1.0f - fg);
+                const float zg = d_g * (1.0f - gg * gg), zo = d_o * og * (1.0f - og);
                 bf16_t *dzp = a.dz + ((long)t * B + b) * G4 + cj;
-                dzp[0] = f32_to_bf16(d_i * ig * (1.0f - ig));
-                dzp[H] = f32_to_bf16(d_f * fg * (1.0f - fg));
-                dzp[2 * H] = f32_to_bf16(d_g * (1.0f - gg * gg));
-                dzp[3 * H] = f32_to_bf16(d_o * og * (1.0f - og));
+                dzp[0] = f32_to_bf16(zi);
+                dzp[H] = f32_to_bf16(zf);
+                dzp[2 * H] = f32_to_bf16(zg);
+                dzp[3 * H] = f32_to_bf16(zo);
+                dbacc[0] += zi;
+                dbacc[1] += zf;
+                dbacc[2] += zg;
+                dbacc[3] += zo;
                 dcn[mb] = d_c * fg;
                 if (s == 0 && a.dc0) a.dc0[(long)b * H + cj] = dcn[mb];
             }
@@ -356,6 +373,22 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
                     a.dh0[(long)bc * H + cj] = f32_to_bf16(v);
             }
             __syncthreads();
+        }
+    }
+    // bias gradient: sum this workgroup's rows (in row order), one partial per XCD
+    {
+        float *dred = &red[0][0][0];                  // 16 x HN x 4 floats fit in red
+        __syncthreads();
+        if (has_cell) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dred[(cr * HN + cu) * 4 + g] = dbacc[g];
+        }
+        __syncthreads();
+        if (tid < 4 * HN) {
+            const int g = tid / HN, u = tid % HN;
+            float v = 0.0f;
+            for (int r = 0; r < 16; ++r) v += dred[(r * HN + u) * 4 + g];
+            a.dbpart[(long)xcd * G4 + g * H + j0 + u] = v;
         }
     }
 }
@@ -442,6 +475,7 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
     a.dz = static_cast<bf16_t *>(bf.dz);
     a.dh0 = static_cast<bf16_t *>(bf.dh0);
     a.dc0 = bf.dc0;
+    a.dbpart = bf.dbpart;
     a.flags = bf.sync + XCD_FLAGS;
     a.timeout = timeout;
     hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
