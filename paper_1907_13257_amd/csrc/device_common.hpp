@@ -84,4 +84,38 @@ __device__ __forceinline__ void mfma32(f32x16 &acc, u32x4 a, u32x4 b, float)
 __device__ __forceinline__ u32x4 ldg16(const void *p) { return *reinterpret_cast<const u32x4 *>(p); }
 __device__ __forceinline__ u32x4 zero16() { return u32x4{0u, 0u, 0u, 0u}; }
 
+// ---------------------------------------------------------------------------
+// Direct global -> LDS loads.  A buffer descriptor covers [base, base+bytes);
+// loads past its end return zero.  buffer_load_dwordx4 ... lds writes lane
+// l's 16 bytes to LDS byte M0 + 16*l, so one wave fills 1 KiB per
+// instruction.  It is issued as inline asm so that the compiler does not
+// wait for it before unrelated LDS accesses; callers order it themselves
+// with s_waitcnt vmcnt and barriers.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ u32x4 buffer_desc(const void *base, long bytes)
+{
+    const unsigned nrec = bytes > 0x7fffffffL ? 0x7fffffffu : (unsigned)bytes;
+    const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+    return u32x4{(unsigned)b, (unsigned)(b >> 32) & 0xffffu, nrec, 0x00020000u};
+}
+
+__device__ __forceinline__ unsigned lds_addr(const void *p) { return (unsigned)(uintptr_t)p; }
+
+__device__ __forceinline__ void dma16(u32x4 rsrc, unsigned lds_byte, unsigned voff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_byte), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt not waited on (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void waitcnt_vm()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | (0x7 << 4) | (0xf << 8) | ((N >> 4) << 14));
+}
+
 }  // namespace lstm355

@@ -246,55 +246,31 @@ __global__ __launch_bounds__(256, (BM * BN > 128 * 128) ? 1 : 2) void gemm_kerne
 // lanes addressing (k = kb + s/4, m = mb + 4 (s % 4)) deliver to lane i the
 // four k values kb..kb+3 of column m = mb + i.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ unsigned lds_addr(const char *p) { return (unsigned)(uintptr_t)p; }
-
-// s_waitcnt vmcnt(N) with expcnt and lgkmcnt not waited on (gfx9 encoding:
-// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
-template <int N>
-__device__ __forceinline__ void waitcnt_vm()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xf) | (0x7 << 4) | (0xf << 8) | ((N >> 4) << 14));
-}
-
-// Buffer -> LDS load of 16 bytes per lane into LDS bytes [lds, lds + 1 KiB).
-// Issued as inline asm so the compiler does not see an LDS write it must wait
-// for before every LDS read; the kernel orders these loads itself with
-// s_waitcnt vmcnt(N) and s_barrier.
-__device__ __forceinline__ void dma16(u32x4 rsrc, unsigned lds_byte, unsigned voff)
-{
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :
-                 : "s"(lds_byte), "v"(voff), "s"(rsrc)
-                 : "memory", "m0");
-}
-
-template <int ROWS, bool KMAJ, int KD>
+template <int ROWS, bool KMAJ, int KD, int NW>
 struct DlLayout {
     static constexpr int RB = KD * 2;             // K-major: bytes per row per stage
     static constexpr int CH = RB / 16;            // K-major: chunks per row
     static constexpr int RW = 256 / RB;           // K-major: rows per 256-byte window
     static constexpr int RP = ROWS * 2;           // M-major: bytes per k-row
     static constexpr int BYTES = ROWS * RB;       // either layout
-    static constexpr int NI = BYTES / 1024 / 4;   // 1 KiB instructions per wave per stage
+    static constexpr int NI = BYTES / 1024 / NW;  // 1 KiB instructions per wave per stage
+    static_assert(NI * 1024 * NW == BYTES, "a stage must split evenly over the waves");
 
     __device__ static __forceinline__ int kslot(int row, int c) { return c ^ ((row / RW) % CH); }
     __device__ static __forceinline__ int mslot(int k, int c) { return c ^ (4 * (k & 3)); }
 };
 
-// One operand of one stage: ROWS rows, KD k.
-template <int ROWS, bool KMAJ, int KD>
+// One operand of one stage: ROWS rows, KD k, loaded by NW waves.
+template <int ROWS, bool KMAJ, int KD, int NW>
 struct DmaOperand {
-    using L = DlLayout<ROWS, KMAJ, KD>;
+    using L = DlLayout<ROWS, KMAJ, KD, NW>;
     u32x4 rsrc;                                   // buffer descriptor (base, limit, format)
     long ld;                                      // elements
     int r0;
 
     __device__ __forceinline__ void init(const char *base, long ld_, int r0_, long bound_bytes)
     {
-        const unsigned nrec = bound_bytes > 0x7fffffffL ? 0x7fffffffu : (unsigned)bound_bytes;
-        const uintptr_t b = reinterpret_cast<uintptr_t>(base);
-        rsrc = u32x4{(unsigned)b, (unsigned)(b >> 32) & 0xffffu, nrec, 0x00020000u};
+        rsrc = buffer_desc(base, bound_bytes);
         ld = ld_;
         r0 = r0_;
     }
@@ -325,7 +301,7 @@ struct DmaOperand {
 template <int ROWS, bool KMAJ, int KD>
 __device__ __forceinline__ unsigned frag_off(int rowbase, int s, int r, int lane)
 {
-    using L = DlLayout<ROWS, KMAJ, KD>;
+    using L = DlLayout<ROWS, KMAJ, KD, 1>;
     if (KMAJ) {
         const int row = rowbase + (lane & 31);
         const int c = 2 * s + (lane >> 5);
@@ -361,13 +337,16 @@ __device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int 
     }
 }
 
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS>
-__global__ __launch_bounds__(256, 1) void gemm_dl_kernel(GemmArgs g)
+// NWM x NWN waves; wave (wm, wn) owns the (BM/NWM) x (BN/NWN) block of the tile.
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN>
+__global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 {
-    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int NW = NWM * NWN;
+    constexpr int WM = BM / NWM, WN = BN / NWN;
     constexpr int FM = WM / 32, FN = WN / 32;
-    using LA = DlLayout<BM, AK, KD>;
-    using LB = DlLayout<BN, BKM, KD>;
+    static_assert(FM * 32 * NWM == BM && FN * 32 * NWN == BN, "wave tiles are multiples of 32");
+    using LA = DlLayout<BM, AK, KD, NW>;
+    using LB = DlLayout<BN, BKM, KD, NW>;
     constexpr int ABYTES = LA::BYTES, STAGE = LA::BYTES + LB::BYTES;
     constexpr int LPW = LA::NI + LB::NI;          // DMA instructions per wave per stage
     extern __shared__ __attribute__((aligned(1024))) char smem[];
@@ -383,10 +362,10 @@ __global__ __launch_bounds__(256, 1) void gemm_dl_kernel(GemmArgs g)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % NWM, wn = wave / NWM;
 
-    DmaOperand<BM, AK, KD> da;
-    DmaOperand<BN, BKM, KD> db;
+    DmaOperand<BM, AK, KD, NW> da;
+    DmaOperand<BN, BKM, KD, NW> db;
     da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)g.K * g.lda * 2);
     db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
 
@@ -476,7 +455,7 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ p
     }
 }
 
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS>
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN>
 hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
 {
     constexpr int LDS = NS * (BM + BN) * KD * 2;
@@ -493,11 +472,11 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.kchunk = ((d.K + splits - 1) / splits + KD - 1) / KD * KD;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
-    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS>;
+    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(256), LDS, s, g);
+    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(64 * NWM * NWN), LDS, s, g);
     e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const long total = (long)d.M * d.N;
@@ -561,7 +540,7 @@ Choice choose(const GemmDesc &d, size_t es)
         int t = std::atoi(env), sp = 1;
         const char *c = std::strchr(env, ',');
         if (c) sp = std::atoi(c + 1);
-        if (t >= 0 && t < 4 && sp >= 1) return Choice{t, sp};
+        if (t >= 0 && t < 9 && sp >= 1) return Choice{t, sp};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
     if (es == 2 && dl_ok(d, 128, 128, 1)) {
@@ -623,31 +602,38 @@ bool dl_ok(const GemmDesc &d, int BM, int BN, int splits)
     return true;
 }
 
+// Largest split count <= want whose fp32 partials fit the caller's split-K workspace.
+int fit_splits(const GemmDesc &d, int want)
+{
+    int sp = want < 1 ? 1 : want;
+    while (sp > 1 && (!d.splitk_ws || (size_t)sp * (size_t)d.M * (size_t)d.N > d.splitk_ws_floats)) --sp;
+    return sp;
+}
+
 template <typename TI, typename TO, bool AK, bool BKM>
 hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
 {
-    const Choice c = choose(d, sizeof(TI));
+    Choice c = choose(d, sizeof(TI));
+    c.splits = fit_splits(d, c.splits);   // also bounds a tuning override
     if constexpr (sizeof(TI) == 4) {
         return launch_gemm<TI, TO, 128, 128, 64, AK, BKM>(d, c.splits, s);
     } else {
-        static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
+        static const int BMs[9] = {256, 256, 128, 128, 256, 128, 256, 128, 256};
+        static const int BNs[9] = {256, 128, 256, 128, 256, 128, 128, 256, 256};
         if (dl_ok(d, BMs[c.tile], BNs[c.tile], c.splits)) {
-            const char *kd = std::getenv("LSTM355_GEMM_KD");
-            const bool deep = kd ? std::atoi(kd) == 64 : false;
-            if (deep && d.K % 64 == 0) {
-                switch (c.tile) {
-                case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 3>(d, c.splits, s);
-                case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 3>(d, c.splits, s);
-                case 3: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4>(d, c.splits, s);
-                default: break;
-                }
-            }
+            const bool k64 = d.K % 64 == 0;
             switch (c.tile) {
-            case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4>(d, c.splits, s);
-            case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 4>(d, c.splits, s);
-            case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 4>(d, c.splits, s);
-            default: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4>(d, c.splits, s);
+            case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 2, 4>(d, c.splits, s);
+            case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 3, 4, 2>(d, c.splits, s);
+            case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 3, 2, 4>(d, c.splits, s);
+            case 4: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 4, 2>(d, c.splits, s);
+            case 5: if (k64) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 2, 2, 2>(d, c.splits, s); break;
+            case 6: if (k64) return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 2, 4, 2>(d, c.splits, s); break;
+            case 7: if (k64) return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 2, 2, 4>(d, c.splits, s); break;
+            case 8: if (k64) return launch_gemm_dl<TO, 256, 256, AK, BKM, 64, 2, 2, 4>(d, c.splits, s); break;
+            default: break;
             }
+            return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, c.splits, s);
         }
         switch (c.tile) {
         case 0: return launch_gemm<TI, TO, 256, 256, 128, AK, BKM>(d, c.splits, s);

@@ -24,6 +24,21 @@ struct Rec {
 std::mutex g_mu;
 bool g_on = false;
 std::vector<Rec> g_recs;
+std::vector<hipEvent_t> g_pool;   // recycled events
+
+// Timing-only events: no system-scope fence (cache write-back) when they
+// complete, so recording them barely perturbs the kernels they bracket.
+hipEvent_t take_event()
+{
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
+    return e;
+}
 
 const char *const kNames[K_NCLASS] = {"gemm_input_proj", "recurrent_fwd", "recurrent_bwd", "gemm_dx",
                                        "gemm_dw",         "gemm_dr",       "gemm_dp",       "small"};
@@ -36,10 +51,10 @@ ProfScope::ProfScope(int kclass, hipStream_t st, double fl, double by) : k(kclas
 {
     std::lock_guard<std::mutex> lk(g_mu);
     if (!g_on) return;
-    hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return;
+    hipEvent_t e = take_event();
+    if (!e) return;
     if (hipEventRecord(e, s) != hipSuccess) {
-        (void)hipEventDestroy(e);
+        g_pool.push_back(e);
         return;
     }
     ev0 = e;
@@ -49,9 +64,11 @@ ProfScope::~ProfScope()
 {
     if (!ev0) return;
     std::lock_guard<std::mutex> lk(g_mu);
-    hipEvent_t e1;
-    if (hipEventCreate(&e1) != hipSuccess || hipEventRecord(e1, s) != hipSuccess) {
-        (void)hipEventDestroy(static_cast<hipEvent_t>(ev0));
+    hipEvent_t e1 = take_event();
+    if (!e1 || hipEventRecord(e1, s) != hipSuccess) {
+        if (e1) g_pool.push_back(e1);
+        (void)hipEventSynchronize(static_cast<hipEvent_t>(ev0));
+        g_pool.push_back(static_cast<hipEvent_t>(ev0));
         return;
     }
     g_recs.push_back(Rec{k, static_cast<hipEvent_t>(ev0), e1, flops, bytes});
@@ -73,8 +90,8 @@ extern "C" lstm_status_t lstm_profile_reset(void)
     std::lock_guard<std::mutex> lk(g_mu);
     for (auto &r : g_recs) {
         (void)hipEventSynchronize(r.b);
-        (void)hipEventDestroy(r.a);
-        (void)hipEventDestroy(r.b);
+        g_pool.push_back(r.a);
+        g_pool.push_back(r.b);
     }
     g_recs.clear();
     return LSTM_OK;

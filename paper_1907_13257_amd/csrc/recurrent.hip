@@ -680,7 +680,7 @@ hipError_t launch_backward(DType t, const RecShape &sh, const RecTiling &tl, con
     if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
     const double flops = 2.0 * sh.T * sh.B * G4 * Hr + (sh.Hp ? 2.0 * sh.T * sh.B * sh.H * sh.Hp : 0.0);
-    const double bytes = (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 8.0 + G4 * (double)es + Hr * (double)es) +
+    const double bytes = (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 4.0 + G4 * (double)es + Hr * (double)es) +
                          G4 * Hr * (double)es + (sh.Hp ? (double)sh.Hp * sh.H * es : 0.0);
     ProfScope ps(K_REC_BWD, s, flops, bytes);
     if (t == DType::BF16)

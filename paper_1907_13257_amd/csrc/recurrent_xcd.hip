@@ -104,6 +104,50 @@ __device__ __forceinline__ bool placed_ok(unsigned *flags, int *s_ok)
     return *s_ok != 0;
 }
 
+// Staging of exchanged rows.  Each wave copies the rows it multiplies (16
+// batch rows, its own k range of RB bytes per row) from the XCD's L2 into its
+// own LDS tile with buffer->LDS loads of whole 128-byte lines, then reads MFMA
+// fragments from the tile.  16-byte chunk c of row r sits at slot
+// c ^ swz(r), which puts the 16 rows one fragment read touches in distinct
+// LDS banks (a 256-byte window of 64 four-byte banks).
+template <int RB>
+__device__ __forceinline__ int stage_swz(int r)
+{
+    if constexpr (RB >= 256)
+        return r & 15;
+    else
+        return (r / (256 / RB)) % (RB / 16);
+}
+
+// Copies rows [r0, r0+16) x bytes [kbyte, kbyte+RB) of a row-major bf16 matrix
+// (row pitch ld elements, descriptor `rs`) into the wave's tile at LDS byte
+// `tile` (16*RB bytes).  Rows past the descriptor's end read as zero.
+template <int RB>
+__device__ __forceinline__ void stage_rows(u32x4 rs, long r0, long ld, int kbyte, unsigned tile, int lane)
+{
+    static_assert(RB % 64 == 0 && (16 * RB) % 1024 == 0, "whole 1 KiB instructions");
+#pragma unroll
+    for (int q = 0; q < 16 * RB / 1024; ++q) {
+        const int o = q * 1024 + lane * 16;
+        const int r = o / RB, p = (o % RB) >> 4;
+        const int c = p ^ stage_swz<RB>(r);
+        const unsigned voff = (unsigned)((r0 + r) * ld * 2 + kbyte + c * 16);
+        dma16(rs, __builtin_amdgcn_readfirstlane(tile + q * 1024), voff);
+    }
+}
+
+// Fragment of 32-deep k chunk `cc` for MFMA operand row lane%16.
+template <int RB>
+__device__ __forceinline__ u32x4 stage_frag(const char *tile, int cc, int lane)
+{
+    const int i = lane & 15;
+    const int slot = (cc * 4 + (lane >> 4)) ^ stage_swz<RB>(i);
+    return *reinterpret_cast<const u32x4 *>(tile + i * RB + slot * 16);
+}
+
+__device__ __forceinline__ void wait_own_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void wait_own_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 struct XFwdArgs {
     int T, B, H, reverse, RX;
     long ldy;
@@ -116,38 +160,45 @@ struct XFwdArgs {
     unsigned long long timeout;
 };
 
-// Waves: kq = wave & 3 takes a quarter of the k chunks, nh = wave >> 2 half
-// of the 4*HN gate rows.  MBX blocks of 16 batch rows per XCD.
+// Wave w multiplies the k range [w*H/8, (w+1)*H/8) for all 4*HN gate rows of
+// the workgroup's cells; the eight partial sums meet in LDS.  MBX blocks of
+// 16 batch rows per XCD.
 template <int HN, int MBX>
 __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 {
     constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
-    constexpr int NBH = NT / 32;      // 16-row blocks per wave half
-    constexpr int KCW = HN / 4;       // 32-wide k chunks per wave (H/32 = HN chunks in all)
+    constexpr int NB = NT / 16;       // 16-row MFMA blocks
+    constexpr int KW = 4 * HN;        // k per wave (H / 8)
+    constexpr int KCW = KW / 32;      // 32-deep chunks per wave
+    constexpr int RB = KW * 2;        // staged bytes per row
     constexpr int NCELL = 16 * HN;    // cells of one row block
-    __shared__ float red[4][16][NT];
+    constexpr int RP = NT + 36;       // padded partial-sum row (conflict-free writes, few read conflicts)
+    __shared__ float red[8][16][RP];
+    __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
     __shared__ int s_ok;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int kq = w & 3, nh = w >> 2;
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
     const int H = a.H, B = a.B;
     const long G4 = 4L * H;
     const int j0 = slot * HN;
     const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
+    const unsigned tile = lds_addr(&stage[w][0]);
 
     if (!placed_ok(a.flags, &s_ok)) return;
 
-    // resident weights: rows of R for this workgroup's cells, this wave's k range
-    u32x4 rf[NBH][KCW];
+    // resident weights: the 4*HN rows of R feeding this workgroup's cells, this wave's k range
+    u32x4 rf[NB][KCW];
 #pragma unroll
-    for (int i = 0; i < NBH; ++i) {
-        const int n = (nh * NBH + i) * 16 + (lane & 15);
+    for (int i = 0; i < NB; ++i) {
+        const int n = i * 16 + (lane & 15);
         const int g = n / HN, u = n % HN;
-        const bf16_t *rrow = a.R + (long)(g * H + j0 + u) * H;
+        const bf16_t *rrow = a.R + (long)(g * H + j0 + u) * H + w * KW;
 #pragma unroll
-        for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + (kq * KCW + c) * 32 + (lane >> 4) * 8);
+        for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + c * 32 + (lane >> 4) * 8);
     }
+    const u32x4 rs_y = buffer_desc(a.y, (long)a.T * B * a.ldy * 2);
+    const u32x4 rs_h0 = buffer_desc(a.h0, (long)B * H * 2);
 
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
@@ -172,41 +223,48 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 #pragma unroll
             for (int g = 0; g < 4; ++g) gx[mb][g] = v ? gp[g * H] : 0.0f;
         }
-        const bf16_t *hp = a.h0;
-        long ldh = H;
+        bool have_h = a.h0 != nullptr;
+        u32x4 rs = rs_h0;
+        long hrow0 = 0, ldh = H;
         if (s > 0) {
             if (!wait_xcd(a.flags, xcd, (unsigned)s, a.timeout, &s_ok)) return;
-            hp = a.y + (long)tprev * B * a.ldy;
+            have_h = true;
+            rs = rs_y;
+            hrow0 = (long)tprev * B;
             ldh = a.ldy;
         }
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
-            f32x4 acc[NBH];
+            f32x4 acc[NB];
 #pragma unroll
-            for (int i = 0; i < NBH; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (hp) {
-                const int b = row0 + mb * 16 + (lane & 15);
+            for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (have_h) {
+                if (mb > 0) wait_own_lds();   // the previous block's fragment reads are done
+                stage_rows<RB>(rs, hrow0 + row0 + mb * 16, ldh, w * KW * 2, tile, lane);
+                wait_own_loads();
                 u32x4 fa[KCW];
 #pragma unroll
-                for (int c = 0; c < KCW; ++c)
-                    fa[c] = b < rowend ? ldg16(hp + (long)b * ldh + (kq * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+                for (int c = 0; c < KCW; ++c) fa[c] = stage_frag<RB>(stage[w], c, lane);
 #pragma unroll
                 for (int c = 0; c < KCW; ++c)
 #pragma unroll
-                    for (int i = 0; i < NBH; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
+                    for (int i = 0; i < NB; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
             }
 #pragma unroll
-            for (int i = 0; i < NBH; ++i)
+            for (int i = 0; i < NB; ++i)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) red[kq][4 * (lane >> 4) + v][(nh * NBH + i) * 16 + (lane & 15)] = acc[i][v];
+                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
             __syncthreads();
             const int b = row0 + mb * 16 + cr;
             if (has_cell && b < rowend) {
                 float z[4];
 #pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    z[g] = red[0][cr][g * HN + cu] + red[1][cr][g * HN + cu] + red[2][cr][g * HN + cu] +
-                           red[3][cr][g * HN + cu] + gx[mb][g];
+                for (int g = 0; g < 4; ++g) {
+                    float v = gx[mb][g];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) v += red[q][cr][g * HN + cu];
+                    z[g] = v;
+                }
                 const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
                 const float c = fg * creg[mb] + ig * gg;
                 const float m = og * tanh_f(c);
@@ -220,9 +278,14 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                 a.y[((long)t * B + b) * a.ldy + cj] = hv;
                 if (last && a.hT) a.hT[(long)b * H + cj] = hv;
             }
-            __syncthreads();
+            // red is rewritten by the next row block; the last block's reads
+            // are ordered by the barrier in publish / wait_xcd instead
+            if (mb + 1 < MBX) __syncthreads();
         }
-        if (!last) publish(a.flags, xcd * WG_PER_XCD + slot, (unsigned)(s + 1));
+        if (!last)
+            publish(a.flags, xcd * WG_PER_XCD + slot, (unsigned)(s + 1));
+        else
+            __syncthreads();
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             const int b = row0 + mb * 16 + cr;
@@ -252,15 +315,26 @@ struct XBwdArgs {
     unsigned long long timeout;
 };
 
-// Waves split the 4H-long reduction of dh_{t-1} = R^T dz_t in eight.
+// Per-cell inputs of one BPTT step (saved forward state and upstream gradient).
+template <int MBX>
+struct BwdIn {
+    float dy[MBX], g[MBX][4], c[MBX], cp[MBX];
+};
+
+// Wave w multiplies the k range [w*H/2, (w+1)*H/2) of dh_{t-1} = R^T dz_t
+// (k over the 4H gate rows); the eight partial sums meet in LDS.
 template <int HN, int MBX>
 __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 {
     constexpr int NBB = HN >= 16 ? HN / 16 : 1;   // 16-column blocks of owned cells
     constexpr int NC = 16 * NBB;
-    constexpr int KCW = HN / 2;                   // 32-wide k chunks per wave (4H/32 = 4*HN in all)
+    constexpr int KW = 16 * HN;                   // k per wave (4H / 8)
+    constexpr int KCW = KW / 32;
+    constexpr int RB = KW * 2;
     constexpr int NCELL = 16 * HN;
-    __shared__ float red[8][16][NC];
+    constexpr int RP = NC + 4;                    // padded partial-sum row (conflict-free writes)
+    __shared__ float red[8][16][RP];
+    __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
     __shared__ int s_ok;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -269,6 +343,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
     const long G4 = 4L * H;
     const int j0 = slot * HN;
     const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
+    const unsigned tile = lds_addr(&stage[w][0]);
 
     if (!placed_ok(a.flags, &s_ok)) return;
 
@@ -277,14 +352,31 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 #pragma unroll
     for (int i = 0; i < NBB; ++i) {
         const int n = i * 16 + (lane & 15);
-        const bf16_t *rrow = a.Rt + (long)(j0 + (n < HN ? n : 0)) * G4;
+        const bf16_t *rrow = a.Rt + (long)(j0 + (n < HN ? n : 0)) * G4 + w * KW;
 #pragma unroll
-        for (int c = 0; c < KCW; ++c)
-            rf[i][c] = n < HN ? ldg16(rrow + (w * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+        for (int c = 0; c < KCW; ++c) rf[i][c] = n < HN ? ldg16(rrow + c * 32 + (lane >> 4) * 8) : zero16();
     }
+    const u32x4 rs_dz = buffer_desc(a.dz, (long)a.T * B * G4 * 2);
 
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
+    auto load_inputs = [&](int s, BwdIn<MBX> &in) {
+        const int t = a.reverse ? a.T - 1 - s : s;
+        const int tp = a.reverse ? t + 1 : t - 1;
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int b = row0 + mb * 16 + cr;
+            const bool v = has_cell && b < rowend;
+            const long rt = (long)t * B + (v ? b : 0);
+            in.dy[mb] = v ? to_f32(a.dy[rt * a.ldy + cj]) : 0.0f;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) in.g[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
+            in.c[mb] = v ? a.cs[rt * H + cj] : 0.0f;
+            in.cp[mb] = (v && s > 0) ? a.cs[((long)tp * B + b) * H + cj]
+                                     : ((v && a.c0) ? a.c0[(long)(v ? b : 0) * H + cj] : 0.0f);
+        }
+    };
+
     float dhn[MBX], dcn[MBX];
     float dbacc[4] = {0.f, 0.f, 0.f, 0.f};   // this thread's rows, summed over steps
 #pragma unroll
@@ -294,35 +386,23 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
         dhn[mb] = (v && a.dhT) ? to_f32(a.dhT[(long)b * H + cj]) : 0.0f;
         dcn[mb] = (v && a.dcT) ? a.dcT[(long)b * H + cj] : 0.0f;
     }
+    BwdIn<MBX> in;
+    load_inputs(a.T - 1, in);
 
     unsigned done = 0;
     for (int s = a.T - 1; s >= 0; --s) {
         const int t = a.reverse ? a.T - 1 - s : s;
-        const int tp = a.reverse ? t + 1 : t - 1;
-        // per-cell inputs of this step (independent of the recurrence)
-        float dyv[MBX], g4[MBX][4], cv[MBX], cpv[MBX];
-#pragma unroll
-        for (int mb = 0; mb < MBX; ++mb) {
-            const int b = row0 + mb * 16 + cr;
-            const bool v = has_cell && b < rowend;
-            const long rt = (long)t * B + b;
-            dyv[mb] = v ? to_f32(a.dy[rt * a.ldy + cj]) : 0.0f;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) g4[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
-            cv[mb] = v ? a.cs[rt * H + cj] : 0.0f;
-            cpv[mb] = v ? (s > 0 ? a.cs[((long)tp * B + b) * H + cj] : (a.c0 ? a.c0[(long)b * H + cj] : 0.0f)) : 0.0f;
-        }
         // gate gradients of the owned cells
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             const int b = row0 + mb * 16 + cr;
             if (has_cell && b < rowend) {
-                const float ig = g4[mb][0], fg = g4[mb][1], gg = g4[mb][2], og = g4[mb][3];
-                const float dm = dyv[mb] + dhn[mb];
-                const float tc = tanh_f(cv[mb]);
+                const float ig = in.g[mb][0], fg = in.g[mb][1], gg = in.g[mb][2], og = in.g[mb][3];
+                const float dm = in.dy[mb] + dhn[mb];
+                const float tc = tanh_f(in.c[mb]);
                 const float d_o = dm * tc;
                 const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
-                const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv[mb];
+                const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * in.cp[mb];
                 const float zi = d_i * ig * (1.0f - ig), zf = d_f * fg * (1.0f - fg);
                 const float zg = d_g * (1.0f - gg * gg), zo = d_o * og * (1.0f - og);
                 bf16_t *dzp = a.dz + ((long)t * B + b) * G4 + cj;
@@ -340,23 +420,24 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
         }
         if (s == 0 && !a.dh0) break;
         publish(a.flags, xcd * WG_PER_XCD + slot, ++done);
+        // the next step's inputs travel while this step's dz is exchanged
+        if (s > 0) load_inputs(s - 1, in);
         if (!wait_xcd(a.flags, xcd, done, a.timeout, &s_ok)) return;
         // dh_{t-1} for the owned cells: dz_t of this XCD's rows times the resident R^T rows
-        const bf16_t *dzt = a.dz + (long)t * B * G4;
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
-            const int b = row0 + mb * 16 + (lane & 15);
-            u32x4 fa[KCW];
-#pragma unroll
-            for (int c = 0; c < KCW; ++c)
-                fa[c] = b < rowend ? ldg16(dzt + (long)b * G4 + (w * KCW + c) * 32 + (lane >> 4) * 8) : zero16();
+            if (mb > 0) wait_own_lds();
+            stage_rows<RB>(rs_dz, (long)t * B + row0 + mb * 16, G4, w * KW * 2, tile, lane);
+            wait_own_loads();
             f32x4 acc[NBB];
 #pragma unroll
             for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < KCW; ++c)
+            for (int c = 0; c < KCW; ++c) {
+                const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
 #pragma unroll
-                for (int i = 0; i < NBB; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
+                for (int i = 0; i < NBB; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
+            }
 #pragma unroll
             for (int i = 0; i < NBB; ++i)
 #pragma unroll
@@ -482,7 +563,7 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
     if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
-                 (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 10.0 + G4 * 2.0) + G4 * sh.H * 2.0);
+                 (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
 #define BWD_CASE(HN_, M_) \
     if (sh.H == 32 * HN_ && m == M_) return coop512(lstm_bwd_xcd<HN_, M_>, s, &a);
