@@ -109,6 +109,17 @@ __device__ __forceinline__ void dma16(u32x4 rsrc, unsigned lds_byte, unsigned vo
                  : "memory", "m0");
 }
 
+// The same at device (agent) scope: the load misses the CU's L1 and reads the
+// L2, so it observes stores other CUs of the same XCD made after an earlier
+// read of the same line.
+__device__ __forceinline__ void dma16_sc1(u32x4 rsrc, unsigned lds_byte, unsigned voff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen sc1 lds"
+                 :
+                 : "s"(lds_byte), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+
 // s_waitcnt vmcnt(N) with expcnt and lgkmcnt not waited on (gfx9 encoding:
 // vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
 template <int N>

@@ -543,6 +543,13 @@ Choice choose(const GemmDesc &d, size_t es)
         if (t >= 0 && t < 9 && sp >= 1) return Choice{t, sp};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
+    if (es == 2 && d.a_kmajor && d.b_kmajor && dl_ok(d, 128, 256, 1)) {
+        // both operands k-contiguous (the input projection): 128x256 tiles of
+        // 8 waves move less L2 traffic per flop than 128x128 once they fill
+        // the 512 workgroup slots at least once
+        const long tiles = (long)((d.M + 127) / 128) * ((d.N + 255) / 256);
+        if (tiles >= 512) return Choice{2, 1};
+    }
     if (es == 2 && dl_ok(d, 128, 128, 1)) {
         // direct-to-LDS 128x128 tiles run two workgroups per CU (512 slots);
         // split K only to fill the slots

@@ -57,6 +57,8 @@ hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
 // Small kernels.
 hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s);  // dst[c][r] = src[r][c]
 hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
+// p[r*ld + c] = v for r < rows, c < cols (16-bit elements).
+hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s);
 // dst[c] (+)= sum_r src[r][c] over a [rows][cols] matrix of element type t, in fp32, deterministic;
 // `partial` holds colsum_partial_floats(rows, cols) floats of scratch.
 size_t colsum_partial_floats(int rows, int cols);

@@ -27,6 +27,21 @@ __global__ void fill_kernel(uint32_t *p, size_t n, uint32_t v)
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// 16-bit fill of a strided row range; 16-byte stores when rows are 8-element aligned.
+__global__ void fill_rows_u16_kernel(uint16_t *p, long rows, int cols, long ld, uint16_t v, int vec)
+{
+    const long per_row = vec ? cols / 8 : cols;
+    const long n = rows * per_row;
+    const unsigned v2 = (unsigned)v | ((unsigned)v << 16);
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
+        const long r = i / per_row, c = i % per_row;
+        if (vec)
+            *reinterpret_cast<u32x4 *>(p + r * ld + c * 8) = u32x4{v2, v2, v2, v2};
+        else
+            p[r * ld + c] = v;
+    }
+}
+
 constexpr int CS_ROWS = 256;   // rows per partial sum
 
 // Pass 1: partial[chunk][c] = sum of rows [chunk*256, chunk*256+256) of column c.
@@ -85,6 +100,16 @@ hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s)
 {
     ProfScope ps(K_SMALL, s, 0.0, 4.0 * n);
     hipLaunchKernelGGL(fill_kernel, dim3(grid_for(n)), dim3(256), 0, s, static_cast<uint32_t *>(p), n, v);
+    return hipGetLastError();
+}
+
+hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s)
+{
+    ProfScope ps(K_SMALL, s, 0.0, 2.0 * rows * cols);
+    const int vec = (cols % 8 == 0 && ld % 8 == 0 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) ? 1 : 0;
+    const size_t n = (size_t)rows * (vec ? cols / 8 : cols);
+    hipLaunchKernelGGL(fill_rows_u16_kernel, dim3(grid_for(n)), dim3(256), 0, s, static_cast<uint16_t *>(p), rows, cols,
+                       ld, v, vec);
     return hipGetLastError();
 }
 

@@ -12,17 +12,15 @@
 // cells (256 KiB at H = 1024, 32 KiB per wave); backward, the HN columns of R
 // (rows of R^T).
 //
-// Exchange protocol per step (no grid barrier, no cache flushes):
-//   producer: plain stores of its cells of h_t (or dz_t) -> wait until every
-//             store of the workgroup has completed -> plain store of its step
-//             counter in the flag array;
-//   consumer: one wave polls the 32 step counters of its XCD with
-//             device-coherent (sc1) loads, which miss the CU's L1; then the
-//             workgroup loads the exchanged rows with plain loads.  Those
-//             addresses are written once per launch and never read before
-//             the step that consumes them, so the CU's L1 cannot hold a stale
-//             copy, and the XCD's L2 holds the producers' data.
-// Polling has a wall-clock watchdog and an abort flag, so every wave exits.
+// Exchange protocol per step (no barrier between workgroups, no flags, no
+// cache flushes): the exchanged rows (y, or dz) are filled with a NOT_READY
+// pattern before the launch, and every element is written exactly once with
+// a plain store.  A consumer wave copies its slice of the rows it needs from
+// L2 into LDS with loads that miss its CU's L1, and repeats the copy until no
+// element of its valid rows still holds NOT_READY.  Nothing is waited on by
+// producers, and a consumer proceeds as soon as the values it uses are
+// there.  Every wait has a wall-clock watchdog and an abort word, so every
+// wave exits.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -41,51 +39,6 @@ constexpr int HWREG_XCC_ID = (31 << 11) | (0 << 6) | 20;   // s_getreg: XCC_ID, 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p)
 {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, 0x7fffffff, 0x00020000);
-}
-
-// Wave 0 polls the step counters of the 32 workgroups of XCD `xcd` until all
-// reach `target`.  Returns false (for the whole workgroup) on abort/timeout.
-__device__ __forceinline__ bool wait_xcd(const unsigned *flags, int xcd, unsigned target, unsigned long long timeout,
-                                         int *s_ok)
-{
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        const __amdgpu_buffer_rsrc_t r = rsrc(flags);
-        const unsigned long long t0 = wall_clock64();
-        int ok = 1;
-        while (true) {
-            unsigned f = target;
-            if (lane < WG_PER_XCD) f = __builtin_amdgcn_raw_buffer_load_b32(r, (xcd * WG_PER_XCD + lane) * 4, 0, 16);
-            unsigned ab = 0;
-            if (lane == 32) ab = __builtin_amdgcn_raw_buffer_load_b32(r, XCD_ABORT * 4, 0, 16);
-            if (__builtin_amdgcn_ballot_w64(ab != 0)) {
-                ok = 0;
-                break;
-            }
-            if (__builtin_amdgcn_ballot_w64(f < target) == 0) break;
-            if (wall_clock64() - t0 > timeout) {
-                if (lane == 0) {
-                    __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __hip_atomic_store(const_cast<unsigned *>(flags) + XCD_ABORT, 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-                }
-                ok = 0;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-        if (lane == 0) *s_ok = ok;
-    }
-    __syncthreads();
-    return *s_ok != 0;
-}
-
-// All of the workgroup's stores have completed, then its step counter is set.
-__device__ __forceinline__ void publish(unsigned *flags, int wg_index, unsigned value)
-{
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (threadIdx.x == 0) flags[wg_index] = value;
 }
 
 // Placement check: this workgroup must run on XCD blockIdx.x % 8.
@@ -122,17 +75,22 @@ __device__ __forceinline__ int stage_swz(int r)
 // Copies rows [r0, r0+16) x bytes [kbyte, kbyte+RB) of a row-major bf16 matrix
 // (row pitch ld elements, descriptor `rs`) into the wave's tile at LDS byte
 // `tile` (16*RB bytes).  Rows past the descriptor's end read as zero.
-template <int RB>
-__device__ __forceinline__ void stage_rows(u32x4 rs, long r0, long ld, int kbyte, unsigned tile, int lane)
+template <int RB, bool COHERENT = false>
+__device__ __forceinline__ void stage_rows(u32x4 rs, long r0, long ld, int kbyte, unsigned tile, int lane,
+                                           unsigned qmask = ~0u)
 {
     static_assert(RB % 64 == 0 && (16 * RB) % 1024 == 0, "whole 1 KiB instructions");
 #pragma unroll
     for (int q = 0; q < 16 * RB / 1024; ++q) {
+        if (!((qmask >> q) & 1u)) continue;   // wave-uniform
         const int o = q * 1024 + lane * 16;
         const int r = o / RB, p = (o % RB) >> 4;
         const int c = p ^ stage_swz<RB>(r);
         const unsigned voff = (unsigned)((r0 + r) * ld * 2 + kbyte + c * 16);
-        dma16(rs, __builtin_amdgcn_readfirstlane(tile + q * 1024), voff);
+        if (COHERENT)
+            dma16_sc1(rs, __builtin_amdgcn_readfirstlane(tile + q * 1024), voff);
+        else
+            dma16(rs, __builtin_amdgcn_readfirstlane(tile + q * 1024), voff);
     }
 }
 
@@ -147,6 +105,74 @@ __device__ __forceinline__ u32x4 stage_frag(const char *tile, int cc, int lane)
 
 __device__ __forceinline__ void wait_own_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 __device__ __forceinline__ void wait_own_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Exchanged bf16 rows are filled with NOT_READY before the launch and each
+// element is written exactly once, never with that pattern (a NaN of that
+// encoding is replaced by the canonical quiet NaN).  A consumer therefore
+// knows an element is final once it reads anything else.
+constexpr bf16_t NOT_READY = 0xffffu;
+
+__device__ __forceinline__ bf16_t ready_value(bf16_t v) { return v == NOT_READY ? (bf16_t)0x7fc0u : v; }
+
+__device__ __forceinline__ bool any_not_ready(u32x4 v)
+{
+    bool r = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r |= (v[e] & 0xffffu) == 0xffffu || (v[e] >> 16) == 0xffffu;
+    return r;
+}
+
+// acc[i] = (16 exchanged rows, this wave's k range) x rf[i] on the matrix
+// cores, once every element of the first `valid` rows is final.  Each attempt
+// copies the wave's slice from the XCD's L2 into its LDS tile (L1 bypassed)
+// and multiplies it while checking for NOT_READY; an attempt that saw one is
+// discarded and repeated.  Returns false if another workgroup aborted or the
+// wall-clock watchdog expired (then the abort word is raised).
+template <int RB, int KCW, int NBX>
+__device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld, int kbyte, unsigned tile,
+                                                     const char *tilep, int lane, int valid,
+                                                     const u32x4 (&rf)[NBX][KCW], f32x4 (&acc)[NBX],
+                                                     unsigned *flags, unsigned long long timeout)
+{
+    constexpr int RPI = 1024 / RB > 0 ? 1024 / RB : 1;   // rows per 1 KiB instruction (RB <= 1024)
+    static_assert(RB <= 1024, "one row per instruction at most");
+    const __amdgpu_buffer_rsrc_t rfl = rsrc(flags);
+    const bool row_in = (lane & 15) < valid;
+    const unsigned long long t0 = wall_clock64();
+    unsigned qmask = ~0u;
+    while (true) {
+        stage_rows<RB, true>(rs, r0, ld, kbyte, tile, lane, qmask);
+        const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+        wait_own_loads();
+#pragma unroll
+        for (int i = 0; i < NBX; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        bool late = false;
+#pragma unroll
+        for (int c = 0; c < KCW; ++c) {
+            const u32x4 fa = stage_frag<RB>(tilep, c, lane);
+            late |= any_not_ready(fa);
+#pragma unroll
+            for (int i = 0; i < NBX; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
+        }
+        const unsigned long long lm = __builtin_amdgcn_ballot_w64(late && row_in);
+        if (lm == 0) return true;
+        // re-copy only the instructions that cover rows still incomplete
+        const unsigned rows = (unsigned)(lm | (lm >> 16) | (lm >> 32) | (lm >> 48)) & 0xffffu;
+        qmask = 0;
+#pragma unroll
+        for (int q = 0; q < 16 / RPI; ++q)
+            if ((rows >> (q * RPI)) & ((1u << RPI) - 1u)) qmask |= 1u << q;
+        if (ab != 0) return false;
+        if (wall_clock64() - t0 > timeout) {
+            if (lane == 0) {
+                __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            return false;
+        }
+        wait_own_lds();
+    }
+}
 
 struct XFwdArgs {
     int T, B, H, reverse, RX;
@@ -209,6 +235,9 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
         creg[mb] = (has_cell && b < rowend && a.c0) ? a.c0[(long)b * H + cj] : 0.0f;
     }
 
+    __shared__ int s_bad;
+    if (tid == 0) s_bad = 0;   // ordered by the first barrier below
+
     int tprev = 0;
     for (int s = 0; s < a.T; ++s) {
         const int t = a.reverse ? a.T - 1 - s : s;
@@ -223,39 +252,34 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 #pragma unroll
             for (int g = 0; g < 4; ++g) gx[mb][g] = v ? gp[g * H] : 0.0f;
         }
-        bool have_h = a.h0 != nullptr;
-        u32x4 rs = rs_h0;
-        long hrow0 = 0, ldh = H;
-        if (s > 0) {
-            if (!wait_xcd(a.flags, xcd, (unsigned)s, a.timeout, &s_ok)) return;
-            have_h = true;
-            rs = rs_y;
-            hrow0 = (long)tprev * B;
-            ldh = a.ldy;
-        }
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             f32x4 acc[NB];
 #pragma unroll
             for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (have_h) {
-                if (mb > 0) wait_own_lds();   // the previous block's fragment reads are done
-                stage_rows<RB>(rs, hrow0 + row0 + mb * 16, ldh, w * KW * 2, tile, lane);
+            const int rb0 = row0 + mb * 16;
+            if (mb > 0) wait_own_lds();   // the previous block's fragment reads are done
+            if (s > 0) {
+                if (!stage_mma_when_ready<RB, KCW, NB>(rs_y, (long)tprev * B + rb0, a.ldy, w * KW * 2, tile, stage[w],
+                                                       lane, rowend - rb0, rf, acc, a.flags, a.timeout))
+                    s_bad = 1;
+            } else if (a.h0) {
+                stage_rows<RB>(rs_h0, rb0, H, w * KW * 2, tile, lane);
                 wait_own_loads();
-                u32x4 fa[KCW];
 #pragma unroll
-                for (int c = 0; c < KCW; ++c) fa[c] = stage_frag<RB>(stage[w], c, lane);
+                for (int c = 0; c < KCW; ++c) {
+                    const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
 #pragma unroll
-                for (int c = 0; c < KCW; ++c)
-#pragma unroll
-                    for (int i = 0; i < NB; ++i) mfma16(acc[i], fa[c], rf[i][c], bf16_t{});
+                    for (int i = 0; i < NB; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
+                }
             }
 #pragma unroll
             for (int i = 0; i < NB; ++i)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
             __syncthreads();
-            const int b = row0 + mb * 16 + cr;
+            if (s_bad) return;   // the same decision in every wave
+            const int b = rb0 + cr;
             if (has_cell && b < rowend) {
                 float z[4];
 #pragma unroll
@@ -269,35 +293,19 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                 const float c = fg * creg[mb] + ig * gg;
                 const float m = og * tanh_f(c);
                 creg[mb] = c;
-                // the saved activations are stored after the step flag is published
-                gx[mb][0] = ig;
-                gx[mb][1] = fg;
-                gx[mb][2] = gg;
-                gx[mb][3] = og;
-                const bf16_t hv = f32_to_bf16(m);
+                const bf16_t hv = ready_value(f32_to_bf16(m));
                 a.y[((long)t * B + b) * a.ldy + cj] = hv;
                 if (last && a.hT) a.hT[(long)b * H + cj] = hv;
-            }
-            // red is rewritten by the next row block; the last block's reads
-            // are ordered by the barrier in publish / wait_xcd instead
-            if (mb + 1 < MBX) __syncthreads();
-        }
-        if (!last)
-            publish(a.flags, xcd * WG_PER_XCD + slot, (unsigned)(s + 1));
-        else
-            __syncthreads();
-#pragma unroll
-        for (int mb = 0; mb < MBX; ++mb) {
-            const int b = row0 + mb * 16 + cr;
-            if (has_cell && b < rowend) {
+                // saved activations for the backward pass (not on the critical path)
                 float *gp = a.gates + ((long)t * B + b) * G4 + cj;
-                gp[0] = gx[mb][0];
-                gp[H] = gx[mb][1];
-                gp[2 * H] = gx[mb][2];
-                gp[3 * H] = gx[mb][3];
-                a.cs[((long)t * B + b) * H + cj] = creg[mb];
-                if (last && a.cT) a.cT[(long)b * H + cj] = creg[mb];
+                gp[0] = ig;
+                gp[H] = fg;
+                gp[2 * H] = gg;
+                gp[3 * H] = og;
+                a.cs[((long)t * B + b) * H + cj] = c;
+                if (last && a.cT) a.cT[(long)b * H + cj] = c;
             }
+            __syncthreads();   // red is rewritten by the next row block or step
         }
         tprev = t;
     }
@@ -388,8 +396,9 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
     }
     BwdIn<MBX> in;
     load_inputs(a.T - 1, in);
+    __shared__ int s_bad;
+    if (tid == 0) s_bad = 0;   // ordered by the first barrier below
 
-    unsigned done = 0;
     for (int s = a.T - 1; s >= 0; --s) {
         const int t = a.reverse ? a.T - 1 - s : s;
         // gate gradients of the owned cells
@@ -406,10 +415,10 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
                 const float zi = d_i * ig * (1.0f - ig), zf = d_f * fg * (1.0f - fg);
                 const float zg = d_g * (1.0f - gg * gg), zo = d_o * og * (1.0f - og);
                 bf16_t *dzp = a.dz + ((long)t * B + b) * G4 + cj;
-                dzp[0] = f32_to_bf16(zi);
-                dzp[H] = f32_to_bf16(zf);
-                dzp[2 * H] = f32_to_bf16(zg);
-                dzp[3 * H] = f32_to_bf16(zo);
+                dzp[0] = ready_value(f32_to_bf16(zi));
+                dzp[H] = ready_value(f32_to_bf16(zf));
+                dzp[2 * H] = ready_value(f32_to_bf16(zg));
+                dzp[3 * H] = ready_value(f32_to_bf16(zo));
                 dbacc[0] += zi;
                 dbacc[1] += zf;
                 dbacc[2] += zg;
@@ -419,31 +428,26 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             }
         }
         if (s == 0 && !a.dh0) break;
-        publish(a.flags, xcd * WG_PER_XCD + slot, ++done);
         // the next step's inputs travel while this step's dz is exchanged
         if (s > 0) load_inputs(s - 1, in);
-        if (!wait_xcd(a.flags, xcd, done, a.timeout, &s_ok)) return;
         // dh_{t-1} for the owned cells: dz_t of this XCD's rows times the resident R^T rows
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
+            const int rb0 = row0 + mb * 16;
             if (mb > 0) wait_own_lds();
-            stage_rows<RB>(rs_dz, (long)t * B + row0 + mb * 16, G4, w * KW * 2, tile, lane);
-            wait_own_loads();
             f32x4 acc[NBB];
 #pragma unroll
             for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int c = 0; c < KCW; ++c) {
-                const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
-#pragma unroll
-                for (int i = 0; i < NBB; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
-            }
+            if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile, stage[w], lane,
+                                                    rowend - rb0, rf, acc, a.flags, a.timeout))
+                s_bad = 1;
 #pragma unroll
             for (int i = 0; i < NBB; ++i)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
             __syncthreads();
-            const int bc = row0 + mb * 16 + cr;
+            if (s_bad) return;   // the same decision in every wave
+            const int bc = rb0 + cr;
             if (has_cell && bc < rowend) {
                 float v = 0.0f;
 #pragma unroll
@@ -532,6 +536,9 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     a.timeout = timeout;
     hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
     if (e != hipSuccess) return e;
+    // the kernel's consumers wait for these elements to change
+    e = fill_rows_u16(bf.y, (long)sh.T * sh.B, sh.H, sh.ldy, NOT_READY, s);
+    if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
                  (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0);
@@ -560,6 +567,9 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
     a.flags = bf.sync + XCD_FLAGS;
     a.timeout = timeout;
     hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+    if (e != hipSuccess) return e;
+    // the kernel's consumers wait for these elements to change
+    e = fill_rows_u16(bf.dz, (long)sh.T * sh.B, 4 * sh.H, 4L * sh.H, NOT_READY, s);
     if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
