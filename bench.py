@@ -30,7 +30,7 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix / vector peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-GEMM_CLASSES = ("gemm_input_proj", "gemm_dx", "gemm_dw", "gemm_dr", "gemm_dp")
+GEMM_CLASSES = ("gemm_input_proj", "gemm_dx", "gemm_dw", "gemm_dr", "gemm_dw_dr", "gemm_dp")
 
 
 def kernel_source_hash() -> str:

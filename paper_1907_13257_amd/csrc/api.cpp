@@ -289,7 +289,30 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             g.A = dz; g.lda = G4; g.B = W; g.ldb = I; g.C = dx; g.ldc = h->ldx;
             TRY_HIP("dx", gemm(g, s, K_GEMM_DX));
         }
-        {  // dW = dZ^T X
+        // [dW | dR] = dZ^T [X | H_prev] as one product when the shapes allow
+        // (H_prev: y of the previous visited step, h0 for the first one)
+        bool fused = false;
+        if (h->dt == DType::BF16 && B % 32 == 0 && T > 1) {
+            GemmDesc g{};
+            g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+            g.M = (int)G4; g.N = I + Hr; g.K = (int)TB;
+            g.A = dz; g.lda = G4; g.B = x; g.ldb = h->ldx; g.C = dW; g.ldc = I; g.beta = accumulate;
+            g.N1 = I;
+            g.B2 = y; g.ldb2 = h->ldy; g.b2_bytes = (long)TB * h->ldy * (long)es;
+            g.B3 = h0; g.ldb3 = Hr; g.b3_bytes = (long)B * Hr * (long)es;
+            if (!d.reverse) {   // k = t*B + b pairs dz_t with y_{t-1} (t >= 1), h0 (t = 0)
+                g.ylo = B; g.yhi = (int)TB; g.yoff = -B; g.hlo = 0;
+            } else {            // dz_t with y_{t+1} (t <= T-2), h0 (t = T-1)
+                g.ylo = 0; g.yhi = (int)TB - B; g.yoff = B; g.hlo = (int)TB - B;
+            }
+            g.hlen = B;
+            g.C2 = dR; g.ldc2 = Hr;
+            if (gemm_dual_ok(g)) {
+                TRY_HIP("dW|dR", gemm(g, s, K_GEMM_DWR));
+                fused = true;
+            }
+        }
+        if (!fused) {  // dW = dZ^T X
             GemmDesc g{};
             g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
             g.M = (int)G4; g.N = I; g.K = (int)TB;
@@ -297,7 +320,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             g.splitk_ws = split_ws; g.splitk_ws_floats = h->split_floats;
             TRY_HIP("dW", gemm(g, s, K_GEMM_DW));
         }
-        {  // dR = sum_t dz_t^T h_{t-1}: steps after the first see y of the previous step, the first sees h0
+        if (!fused) {  // dR = sum_t dz_t^T h_{t-1}: steps after the first see y of the previous step, the first sees h0
             int beta = accumulate;
             const char *dzc = static_cast<const char *>(dz);
             const char *yc = static_cast<const char *>(y);

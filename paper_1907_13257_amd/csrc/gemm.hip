@@ -36,6 +36,13 @@ struct GemmArgs {
     int tiles_n, ntiles, per_xcd;
     int kchunk;                  // K per split (multiple of the stage depth)
     float *partial;              // split > 1: fp32 partials [split][M][N]
+    // second column block (see GemmDesc)
+    int N1;
+    const char *B2, *B3;
+    long ldb2, ldb3, b2_bytes, b3_bytes;
+    int ylo, yhi, yoff, hlo, hlen;
+    char *C2;
+    long ldc2;
 };
 
 // Global -> register -> LDS staging of one operand for one K stage.
@@ -356,8 +363,15 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     if (tile >= g.ntiles) return;
     const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
-    const int kbeg = blockIdx.y * g.kchunk;
-    const int kend = min(g.K, kbeg + g.kchunk);
+    // second column block: its own B operand segments, k range and output
+    constexpr bool DUAL_OK = !AK && !BKM;
+    const bool second = DUAL_OK && g.N1 > 0 && n0 >= g.N1;
+    int kbeg = blockIdx.y * g.kchunk;
+    int kend = min(g.K, kbeg + g.kchunk);
+    if (second && !g.B3) {   // no h0 segment: only the B2 range contributes
+        kbeg = g.ylo;
+        kend = g.yhi;
+    }
     const int nst = (kend - kbeg) / KD;
 
     const int tid = threadIdx.x;
@@ -365,9 +379,23 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     const int wm = wave % NWM, wn = wave / NWM;
 
     DmaOperand<BM, AK, KD, NW> da;
-    DmaOperand<BN, BKM, KD, NW> db;
+    DmaOperand<BN, BKM, KD, NW> db;    // B, or B2 for the second block
+    DmaOperand<BN, BKM, KD, NW> dh;    // B3 (second block only)
     da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)g.K * g.lda * 2);
-    db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
+    if (!second) {
+        db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
+    } else {
+        db.init(g.B2, g.ldb2, n0 - g.N1, g.b2_bytes);
+        dh.init(g.B3 ? g.B3 : g.B2, g.ldb3, n0 - g.N1, g.B3 ? g.b3_bytes : 0);
+    }
+    auto issue_b = [&](unsigned dst, int k0) {
+        if (!second)
+            db.issue(dst, k0, wave, lane);
+        else if (k0 >= g.hlo && k0 < g.hlo + g.hlen)
+            dh.issue(dst, k0 - g.hlo, wave, lane);
+        else
+            db.issue(dst, k0 + g.yoff, wave, lane);
+    };
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -383,7 +411,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
         if (s < nst) {
             const unsigned st_base = sbase + s * STAGE;
             da.issue(st_base, kbeg + s * KD, wave, lane);
-            db.issue(st_base + ABYTES, kbeg + s * KD, wave, lane);
+            issue_b(st_base + ABYTES, kbeg + s * KD);
         }
 
     for (int st = 0; st < nst; ++st) {
@@ -396,7 +424,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
         if (st + NS - 1 < nst) {
             const unsigned st_base = sbase + ((st + NS - 1) % NS) * STAGE;
             da.issue(st_base, kbeg + (st + NS - 1) * KD, wave, lane);
-            db.issue(st_base + ABYTES, kbeg + (st + NS - 1) * KD, wave, lane);
+            issue_b(st_base + ABYTES, kbeg + (st + NS - 1) * KD);
         }
         const char *abase = smem + (st % NS) * STAGE;
         const char *bbase = abase + ABYTES;
@@ -414,6 +442,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 
     const bool split = g.partial != nullptr;
     float *part = split ? g.partial + (long)blockIdx.y * g.M * g.N : nullptr;
+    TO *cbase = reinterpret_cast<TO *>(second ? g.C2 : g.C);
+    const long ldc = second ? g.ldc2 : g.ldc;
+    const int coff = second ? g.N1 : 0;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -428,7 +459,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
                     if (split) {
                         part[(long)row * g.N + col] = acc[i][j][v];
                     } else {
-                        TO *cp = reinterpret_cast<TO *>(g.C) + (long)row * g.ldc + col;
+                        TO *cp = cbase + (long)row * ldc + (col - coff);
                         float r = acc[i][j][v] + bv;
                         if (g.beta) r += to_f32(*cp);
                         *cp = from_f32<TO>(r);
@@ -472,6 +503,11 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.kchunk = ((d.K + splits - 1) / splits + KD - 1) / KD * KD;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
+    g.N1 = d.N1;
+    g.B2 = static_cast<const char *>(d.B2); g.ldb2 = d.ldb2; g.b2_bytes = d.b2_bytes;
+    g.B3 = static_cast<const char *>(d.B3); g.ldb3 = d.ldb3; g.b3_bytes = d.b3_bytes;
+    g.ylo = d.ylo; g.yhi = d.yhi; g.yoff = d.yoff; g.hlo = d.hlo; g.hlen = d.hlen;
+    g.C2 = static_cast<char *>(d.C2); g.ldc2 = d.ldc2;
     auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
@@ -505,6 +541,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     g.kchunk = ((d.K + splits - 1) / splits + KS - 1) / KS * KS;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
+    g.N1 = 0; g.B2 = g.B3 = nullptr; g.C2 = nullptr;
     auto kern = gemm_kernel<TI, TO, BM, BN, KB, AK, BKM>;
     if (LDS > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
@@ -620,6 +657,13 @@ int fit_splits(const GemmDesc &d, int want)
 template <typename TI, typename TO, bool AK, bool BKM>
 hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
 {
+    if constexpr (sizeof(TI) == 2 && !AK && !BKM) {
+        if (d.N1 > 0) {   // two column blocks: 128x128 tiles, no split
+            if (!dl_ok(d, 128, 128, 1) || d.N1 % 128) return hipErrorInvalidValue;
+            return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, 1, s);
+        }
+    }
+    if (d.N1 > 0) return hipErrorInvalidValue;
     Choice c = choose(d, sizeof(TI));
     c.splits = fit_splits(d, c.splits);   // also bounds a tuning override
     if constexpr (sizeof(TI) == 4) {
@@ -665,13 +709,31 @@ hipError_t dispatch_layout(const GemmDesc &d, hipStream_t s)
 
 }  // namespace
 
+bool gemm_dual_ok(const GemmDesc &d)
+{
+    if (d.in != DType::BF16 || d.a_kmajor || d.b_kmajor || !d.out_f32) return false;
+    if (d.N1 <= 0 || d.N1 >= d.N || d.N1 % 128 || d.N % 128 || d.M % 128 || d.K % 32) return false;
+    if (d.ylo % 32 || d.yhi % 32 || d.hlo % 32 || d.hlen % 32 || d.ylo < 0 || d.yhi > d.K || d.ylo >= d.yhi)
+        return false;
+    if (d.B3 && (d.hlo < 0 || d.hlo + d.hlen > d.K)) return false;
+    return dl_ok(d, 128, 128, 1);
+}
+
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
 {
     if (d.M <= 0 || d.N <= 0 || d.K <= 0) return hipSuccess;
-    const double flops = 2.0 * d.M * d.N * (double)d.K;
     const double es = (double)dsize(d.in);
-    const double bytes = es * ((double)d.M * d.K + (double)d.N * d.K) +
-                         (d.out_f32 ? 4.0 : es) * (double)d.M * d.N * (d.beta ? 2.0 : 1.0);
+    double flops, bytes;
+    if (d.N1 > 0) {   // second column block over its own k range
+        const double k2 = (double)(d.yhi - d.ylo) + (d.B3 ? d.hlen : 0);
+        flops = 2.0 * d.M * ((double)d.N1 * d.K + (double)(d.N - d.N1) * k2);
+        bytes = es * ((double)d.M * d.K + (double)d.N1 * d.K + (double)(d.N - d.N1) * k2) +
+                4.0 * d.M * d.N * (d.beta ? 2.0 : 1.0);
+    } else {
+        flops = 2.0 * d.M * d.N * (double)d.K;
+        bytes = es * ((double)d.M * d.K + (double)d.N * d.K) +
+                (d.out_f32 ? 4.0 : es) * (double)d.M * d.N * (d.beta ? 2.0 : 1.0);
+    }
     ProfScope ps(kclass, s, flops, bytes);
     return d.in == DType::BF16 ? dispatch_layout<bf16_t>(d, s) : dispatch_layout<float>(d, s);
 }

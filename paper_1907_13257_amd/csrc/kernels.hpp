@@ -21,6 +21,7 @@ enum KClass {
     K_GEMM_DR,       // dR = dZ^T H_prev
     K_GEMM_DP,       // dP = dH^T M
     K_SMALL,         // transposes, column sums, fills, adds
+    K_GEMM_DWR,      // [dW | dR] = dZ^T [X | H_prev] as one product
     K_NCLASS
 };
 const char *kclass_name(int k);
@@ -51,8 +52,22 @@ struct GemmDesc {
     int beta;
     float *splitk_ws;          // optional fp32 scratch for split-K partials
     size_t splitk_ws_floats;
+    // Optional second column block (bf16, both operands m-major only): columns
+    // n >= N1 of the product use B2 / B3 instead of B and are written to C2:
+    //   C2[m][n-N1] (+)= sum over k of A(m,k) * S(n-N1, k), where row k of the
+    //   operand S is B3 row (k - hlo) for k in [hlo, hlo+hlen) (skipped when
+    //   B3 is NULL) and B2 row (k + yoff) for k in [ylo, yhi).
+    // Stages of 32 k never straddle those ranges (hlo, hlen, ylo, yhi are
+    // multiples of 32).
+    int N1 = 0;                // 0: no second block
+    const void *B2 = nullptr; long ldb2 = 0; long b2_bytes = 0;
+    const void *B3 = nullptr; long ldb3 = 0; long b3_bytes = 0;
+    int ylo = 0, yhi = 0, yoff = 0, hlo = 0, hlen = 0;
+    void *C2 = nullptr; long ldc2 = 0;
 };
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
+// Whether a descriptor with a second column block (N1 > 0) can run.
+bool gemm_dual_ok(const GemmDesc &d);
 
 // Small kernels.
 hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s);  // dst[c][r] = src[r][c]

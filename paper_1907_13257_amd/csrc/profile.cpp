@@ -41,7 +41,8 @@ hipEvent_t take_event()
 }
 
 const char *const kNames[K_NCLASS] = {"gemm_input_proj", "recurrent_fwd", "recurrent_bwd", "gemm_dx",
-                                       "gemm_dw",         "gemm_dr",       "gemm_dp",       "small"};
+                                       "gemm_dw",         "gemm_dr",       "gemm_dp",       "small",
+                                       "gemm_dw_dr"};
 
 }  // namespace
 

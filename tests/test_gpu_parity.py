@@ -121,6 +121,10 @@ LAYER_CASES = [
     (3, 500, 40, 256, 0, "bf16", False),   # 63 rows per XCD: four row blocks
     (5, 16, 48, 1024, 0, "bf16", False),   # 2 rows per XCD, full-width cells
     (1, 9, 16, 256, 0, "bf16", True),      # a single step
+    # [dW | dR] as one product (bf16, B a multiple of 32, I and I + H multiples of 128)
+    (4, 32, 128, 256, 0, "bf16", False),   # with h0: the first step's segment comes from h0
+    (3, 64, 128, 256, 0, "bf16", True),    # reverse: h0 pairs with the last time index
+    (5, 32, 256, 128, 0, "bf16", False),   # generic recurrence kernels
 ]
 
 XCD_VARIANT = 1000
@@ -146,6 +150,25 @@ def test_layer_without_initial_state_or_final_grads():
     gpu = run_layer_gpu(c, T, B, I, H, 0, "f32", False)
     ref = oracle_layer(c, 0, False)
     check_layer(gpu, ref, "f32", "zero states")
+
+
+def test_fused_weight_gradients_without_h0_and_accumulating():
+    """[dW | dR] as one product with no initial state (the first step's
+    segment is skipped), then accumulated into existing gradients."""
+    T, B, I, H = 4, 32, 128, 256
+    for reverse in (False, True):
+        announce(f"fused dW|dR zero state rev{int(reverse)}")
+        c = layer_case(T, B, I, H, 0, "bf16", reverse, seed=11 + reverse, states=False, final_grads=False)
+        gpu = run_layer_gpu(c, T, B, I, H, 0, "bf16", reverse)
+        ref = oracle_layer(c, 0, reverse)
+        check_layer(gpu, ref, "bf16", f"fused zero state rev{int(reverse)}")
+        rng = np.random.default_rng(3)
+        prior = dict(dW=rng.standard_normal((4 * H, I)), dR=rng.standard_normal((4 * H, H)),
+                     db=rng.standard_normal(4 * H))
+        prior = {k: v.astype(np.float32).astype(np.float64) for k, v in prior.items()}
+        gpu = run_layer_gpu(c, T, B, I, H, 0, "bf16", reverse, accumulate_into=prior)
+        for k in ("dW", "dR", "db"):
+            assert normwise(gpu[k], ref[k] + prior[k]) <= TOL["bf16"]["grad"], k
 
 
 def test_gradient_accumulation():
