@@ -16,7 +16,7 @@ LIB = os.path.join(HERE, "liblstm355.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm.hip", "recurrent.hip", "recurrent_xcd.hip", "pointwise.hip", "profile.cpp", "api.cpp"]
+SOURCES = ["gemm.hip", "recurrent.hip", "recurrent_xcd.hip", "pointwise.hip", "profile.cpp", "stepwise.cpp", "api.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result", "-Wno-unused-value",
           f"--offload-arch={ARCH}",

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 
@@ -74,6 +75,20 @@ lstm_status_t ensure_plan(lstm_handle *h)
     h->num_cus = cus;
     h->dev = dev;
     return LSTM_OK;
+}
+
+// Recurrence implementation for this handle: the persistent kernels keep
+// the recurrent weights on chip; the stepwise sequence streams them per step
+// and is used for LSTMP layers with wide cells (BigLSTM: 8192 cells) and
+// whenever no persistent tiling fits.  LSTM355_RECURRENCE=stepwise or
+// =persistent overrides the choice (testing and tuning).
+bool use_stepwise(const lstm_handle *h, bool persistent_ok)
+{
+    const char *env = std::getenv("LSTM355_RECURRENCE");
+    if (env && std::strcmp(env, "stepwise") == 0) return true;
+    if (env && std::strcmp(env, "persistent") == 0 && persistent_ok) return false;
+    if (!persistent_ok) return true;
+    return h->d.Hp > 0 && h->d.H >= 2048;
 }
 
 #define TRY_HIP(what, expr)                                  \
@@ -189,10 +204,6 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
             if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
         lstm_status_t st = ensure_plan(h);
         if (st != LSTM_OK) return st;
-        if (!h->fwd_ok) {
-            std::snprintf(g_detail, sizeof(g_detail), "no forward tiling fits this device");
-            return LSTM_ERR_UNSUPPORTED;
-        }
         hipStream_t s = static_cast<hipStream_t>(stream);
         char *rv = static_cast<char *>(reserve);
         char *wv = static_cast<char *>(workspace);
@@ -215,10 +226,15 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
         fb.ms = d.Hp ? rv + h->r_ms : nullptr;
         fb.y = y; fb.hT = hT; fb.cT = cT;
         fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        if (xcd_path_ok(h->dt, sh, h->num_cus))
+        const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+        if (!xcd && use_stepwise(h, h->fwd_ok)) {
+            StepwiseArgs sw{R, P, reinterpret_cast<float *>(wv + h->w_split), h->split_floats};
+            TRY_HIP("forward recurrence (stepwise)", forward_stepwise(h->dt, sh, fb, sw, s));
+        } else if (xcd) {
             TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s));
-        else
+        } else {
             TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
+        }
         return LSTM_OK;
     } catch (...) {
         return invalid("exception");
@@ -246,10 +262,6 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
         lstm_status_t st = ensure_plan(h);
         if (st != LSTM_OK) return st;
-        if (!h->bwd_ok) {
-            std::snprintf(g_detail, sizeof(g_detail), "no backward tiling fits this device");
-            return LSTM_ERR_UNSUPPORTED;
-        }
         hipStream_t s = static_cast<hipStream_t>(stream);
         const char *rv = static_cast<const char *>(reserve);
         char *wv = static_cast<char *>(workspace);
@@ -262,10 +274,14 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         void *dH = Hp ? wv + h->w_dH : nullptr;
         float *split_ws = reinterpret_cast<float *>(wv + h->w_split);
 
-        TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s));
-        if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
-
         RecShape sh{T, B, I, H, Hp, d.reverse, h->ldy};
+        const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+        const bool stepwise = !xcd && use_stepwise(h, h->bwd_ok);
+        if (!stepwise) {   // the persistent kernels keep rows of R^T (and P^T)
+            TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s));
+            if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
+        }
+
         BwdBufs bb{};
         bb.Rt = Rt; bb.Pt = Pt; bb.dy = dy; bb.dhT = dhT; bb.dcT = dcT; bb.h0 = h0; bb.c0 = c0;
         bb.gates = reinterpret_cast<const float *>(rv + h->r_gates);
@@ -276,11 +292,14 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         bb.dh0 = dh0; bb.dc0 = dc0;
         bb.dbpart = reinterpret_cast<float *>(wv + h->w_part);
         bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
-        if (xcd)
+        if (stepwise) {
+            StepwiseArgs sw{R, P, split_ws, h->split_floats};
+            TRY_HIP("backward recurrence (stepwise)", backward_stepwise(h->dt, sh, bb, sw, s));
+        } else if (xcd) {
             TRY_HIP("backward recurrence (XCD-local)", launch_backward_xcd(sh, bb, watchdog_ticks(), s));
-        else
+        } else {
             TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
+        }
 
         if (dx) {  // dX = dZ W
             GemmDesc g{};
@@ -411,7 +430,14 @@ extern "C" lstm_status_t lstm_describe_tiling(lstm_handle_t h, int *out8)
     lstm_status_t st = ensure_plan(h);
     if (st != LSTM_OK) return st;
     RecShape sh{h->d.T, h->d.B, h->d.I, h->d.H, h->d.Hp, h->d.reverse, h->ldy};
-    if (xcd_path_ok(h->dt, sh, h->num_cus)) {
+    const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+    if (!xcd && use_stepwise(h, h->fwd_ok && h->bwd_ok)) {
+        // stepwise sequence: GEMM launches per step, no persistent grid
+        const int v[8] = {0, 0, h->d.B, STEPWISE_VARIANT, 0, 0, h->d.B, STEPWISE_VARIANT};
+        for (int i = 0; i < 8; ++i) out8[i] = v[i];
+        return LSTM_OK;
+    }
+    if (xcd) {
         // XCD-local kernels: 256 workgroups, H/32 cells each, ceil(B/8) rows per XCD
         const int rx = (h->d.B + 7) / 8;
         const int v[8] = {256, h->d.H / 32, rx, XCD_VARIANT, 256, h->d.H / 32, rx, XCD_VARIANT};

@@ -19,6 +19,7 @@
 #include "device_common.hpp"
 #include "kernels.hpp"
 
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 
@@ -345,7 +346,8 @@ __device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int 
 }
 
 // NWM x NWN waves; wave (wm, wn) owns the (BM/NWM) x (BN/NWN) block of the tile.
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN>
+// CB: the instantiation used when C is accumulated into (beta = 1, no split).
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false>
 __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 {
     constexpr int NW = NWM * NWN;
@@ -445,6 +447,34 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     TO *cbase = reinterpret_cast<TO *>(second ? g.C2 : g.C);
     const long ldc = second ? g.ldc2 : g.ldc;
     const int coff = second ? g.N1 : 0;
+    // beta, CB instantiations: C is read block by block before anything is
+    // stored (a load may not pass an earlier store to C in program order, so
+    // interleaving them would expose one memory latency per element).  The
+    // other instantiations add C element by element: the staging registers
+    // would lower their occupancy.
+    constexpr bool CPRE = CB;
+    if (CPRE && !split && g.beta) {
+        constexpr int CJ = 1;   // one 32x32 block (16 values) per batch of loads
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j0 = 0; j0 < FN; j0 += CJ) {
+                float cv[CJ][16];
+#pragma unroll
+                for (int j = 0; j < CJ; ++j) {
+                    const int col = n0 + wn * WN + (j0 + j) * 32 + (lane & 31);
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                        cv[j][v] = (row < g.M && col < g.N) ? to_f32(cbase[(long)row * ldc + (col - coff)]) : 0.0f;
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < CJ; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j0 + j][v] += cv[j][v];
+            }
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -461,7 +491,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
                     } else {
                         TO *cp = cbase + (long)row * ldc + (col - coff);
                         float r = acc[i][j][v] + bv;
-                        if (g.beta) r += to_f32(*cp);
+                        if (!CPRE && g.beta) r += to_f32(*cp);
                         *cp = from_f32<TO>(r);
                     }
                 }
@@ -486,7 +516,62 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ p
     }
 }
 
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN>
+// The same four columns at a time (N and ldc multiples of 4, C 16-byte
+// aligned), with the split loop unrolled so that several partial loads are in
+// flight per thread.
+template <typename TO>
+__global__ __launch_bounds__(256) void splitk_reduce4(const float *__restrict__ partial, int splits, int M, int N,
+                                                       const float *bias, int beta, TO *C, long ldc)
+{
+    const long total = (long)M * N, total4 = total / 4;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < total4; i += (long)gridDim.x * 256) {
+        const long e = i * 4;
+        const int m = (int)(e / N), n = (int)(e % N);
+        f32x4 r = {0.f, 0.f, 0.f, 0.f};
+        int sp = 0;
+        for (; sp + 4 <= splits; sp += 4) {
+            const f32x4 a = *reinterpret_cast<const f32x4 *>(partial + (long)sp * total + e);
+            const f32x4 b = *reinterpret_cast<const f32x4 *>(partial + (long)(sp + 1) * total + e);
+            const f32x4 c = *reinterpret_cast<const f32x4 *>(partial + (long)(sp + 2) * total + e);
+            const f32x4 d = *reinterpret_cast<const f32x4 *>(partial + (long)(sp + 3) * total + e);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) r[v] = r[v] + a[v] + b[v] + c[v] + d[v];
+        }
+        for (; sp < splits; ++sp) {
+            const f32x4 a = *reinterpret_cast<const f32x4 *>(partial + (long)sp * total + e);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) r[v] += a[v];
+        }
+        TO *cp = C + (long)m * ldc + n;
+        if (beta) {   // all four loads before the first store
+            float c4[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) c4[v] = to_f32(cp[v]);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) r[v] += c4[v];
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) cp[v] = from_f32<TO>(bias ? r[v] + bias[n + v] : r[v]);
+    }
+}
+
+template <typename TO>
+hipError_t launch_splitk_reduce(const GemmDesc &d, int splits, hipStream_t s)
+{
+    const long total = (long)d.M * d.N;
+    const bool vec = d.N % 4 == 0 && d.ldc % 4 == 0 && (reinterpret_cast<uintptr_t>(d.C) & 15) == 0;
+    long grid = ((vec ? total / 4 : total) + 255) / 256;
+    if (grid > 4096) grid = 4096;
+    if (vec)
+        hipLaunchKernelGGL(splitk_reduce4<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
+                           d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
+    else
+        hipLaunchKernelGGL(splitk_reduce<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
+                           d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
+    return hipGetLastError();
+}
+
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false>
 hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
 {
     constexpr int LDS = NS * (BM + BN) * KD * 2;
@@ -508,19 +593,14 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.B3 = static_cast<const char *>(d.B3); g.ldb3 = d.ldb3; g.b3_bytes = d.b3_bytes;
     g.ylo = d.ylo; g.yhi = d.yhi; g.yoff = d.yoff; g.hlo = d.hlo; g.hlen = d.hlen;
     g.C2 = static_cast<char *>(d.C2); g.ldc2 = d.ldc2;
-    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN>;
+    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN, CB>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(64 * NWM * NWN), LDS, s, g);
     e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
-    const long total = (long)d.M * d.N;
-    long grid = (total + 255) / 256;
-    if (grid > 4096) grid = 4096;
-    hipLaunchKernelGGL(splitk_reduce<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
-                       d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
-    return hipGetLastError();
+    return launch_splitk_reduce<TO>(d, splits, s);
 }
 
 template <typename TI, typename TO, int BM, int BN, int KB, bool AK, bool BKM>
@@ -551,12 +631,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(256), LDS, s, g);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
-    const long total = (long)d.M * d.N;
-    long grid = (total + 255) / 256;
-    if (grid > 4096) grid = 4096;
-    hipLaunchKernelGGL(splitk_reduce<TO>, dim3((unsigned)grid), dim3(256), 0, s, d.splitk_ws, splits, d.M, d.N,
-                       d.bias, d.beta, reinterpret_cast<TO *>(d.C), d.ldc);
-    return hipGetLastError();
+    return launch_splitk_reduce<TO>(d, splits, s);
 }
 
 // Tile and split choice: a crude model of per-CU efficiency per tile shape,
@@ -566,18 +641,65 @@ struct Choice {
     int splits;
 };
 
+// Tile configurations of the direct-to-LDS kernel (bf16):
+//   index: BM x BN, waves (NWM x NWN), k per stage, ring stages
+//   0: 256x256, 2x4, 32, 4      1: 256x128, 4x2, 32, 3    2: 128x256, 2x4, 32, 3
+//   3: 128x128, 2x2, 32, 4      4: 256x256, 4x2, 32, 4    5: 128x128, 2x2, 64, 2
+//   6: 256x128, 4x2, 64, 2      7: 128x256, 2x4, 64, 2    8: 256x256, 2x4, 64, 2
+//   9: 256x256, 2x2, 32, 4     10: 256x256, 2x2, 64, 2   11: 128x256, 2x2, 32, 3
+//  12: 256x128, 2x2, 32, 3     13: 128x256, 2x4, 64, 3   14: 256x128, 4x2, 64, 3
+//  15: 128x128, 2x2, 64, 3     16: 128x128, 2x2, 64, 4   17: 128x128, 2x2, 32, 8
+// (16 and 17 keep 96 / 112 KiB of operands in flight per workgroup: the
+// per-step recurrent products stream their weights from HBM once)
+constexpr int NTILES = 18;
+const int kTileBM[NTILES] = {256, 256, 128, 128, 256, 128, 256, 128, 256, 256, 256, 128, 256, 128, 256, 128, 128, 128};
+const int kTileBN[NTILES] = {256, 128, 256, 128, 256, 128, 128, 256, 256, 256, 256, 256, 128, 256, 128, 128, 128, 128};
+const int kTileKD[NTILES] = {32, 32, 32, 32, 32, 64, 64, 64, 64, 32, 64, 32, 32, 64, 64, 64, 64, 32};
+// Workgroups of each configuration that fit on one CU (LDS-limited).
+const int kTileSlots[NTILES] = {1, 1, 1, 2, 1, 2, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, 1};
+
 bool dl_ok(const GemmDesc &d, int BM, int BN, int splits);
+bool env_choice(Choice *c);
+
+// Split count for tile shape BM x BN with `slots` workgroups per CU: enough
+// k splits to fill the CUs, against the cost of the fp32 partials.
+int model_splits(const GemmDesc &d, int BM, int BN, int slots, int kd)
+{
+    const double cu_rate = 4096.0 * 2.4e9 * 0.35;
+    const long tiles = (long)((d.M + BM - 1) / BM) * ((d.N + BN - 1) / BN);
+    int best = 1;
+    double best_t = 1e30;
+    for (int sp = 1; sp <= 64; sp *= 2) {
+        if (sp > 1 && (!d.splitk_ws || (size_t)sp * d.M * d.N > d.splitk_ws_floats)) break;
+        if (sp > 1 && d.K / sp < 4 * kd) break;
+        const long items = tiles * sp;
+        const long waves = (items + 256L * slots - 1) / (256L * slots);
+        double tt = waves * 2.0 * BM * BN * ((double)d.K / sp) / (cu_rate / slots);
+        if (sp > 1) tt += ((double)sp + 1.0) * d.M * d.N * 4.0 / 5.0e12 + 3e-6;
+        if (tt < best_t * 0.97) {
+            best_t = tt;
+            best = sp;
+        }
+    }
+    return best;
+}
 
 Choice choose(const GemmDesc &d, size_t es)
 {
     static const int BMs[4] = {256, 256, 128, 128}, BNs[4] = {256, 128, 256, 128};
     static const double eff[4] = {1.0, 0.8, 0.8, 0.55};
-    const char *env = std::getenv("LSTM355_GEMM_TILE");   // tuning override: "tile,splits"
-    if (env) {
-        int t = std::atoi(env), sp = 1;
-        const char *c = std::strchr(env, ',');
-        if (c) sp = std::atoi(c + 1);
-        if (t >= 0 && t < 9 && sp >= 1) return Choice{t, sp};
+    {
+        Choice c;
+        if (env_choice(&c)) {   // tuning override; a tile without a split count gets the modelled one
+            if (c.splits == 0) c.splits = model_splits(d, kTileBM[c.tile], kTileBN[c.tile], kTileSlots[c.tile],
+                                                       kTileKD[c.tile]);
+            return c;
+        }
+    }
+    if (es == 2 && d.M <= 256 && d.K % 64 == 0 && dl_ok(d, 128, 128, 1)) {
+        // skinny products (one step of the stepwise recurrence) stream their
+        // weight operand once: deep rings keep enough of it in flight
+        return Choice{16, model_splits(d, 128, 128, 1, 64)};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
     if (es == 2 && d.a_kmajor && d.b_kmajor && dl_ok(d, 128, 256, 1)) {
@@ -593,9 +715,9 @@ Choice choose(const GemmDesc &d, size_t es)
         Choice best{3, 1};
         double best_t = 1e30;
         const long tiles = (long)((d.M + 127) / 128) * ((d.N + 127) / 128);
-        for (int sp = 1; sp <= 8; sp *= 2) {
+        for (int sp = 1; sp <= 64; sp *= 2) {   // skinny products (per-step recurrences) split K widely
             if (sp > 1 && (!d.splitk_ws || (size_t)sp * d.M * d.N > d.splitk_ws_floats)) break;
-            if (sp > 1 && d.K / sp < 512) break;
+            if (sp > 1 && d.K / sp < 256) break;
             const long items = tiles * sp;
             const long waves = (items + 511) / 512;
             double tt = waves * 2.0 * 128 * 128 * ((double)d.K / sp) / (cu_rate * 0.5);
@@ -649,18 +771,85 @@ bool dl_ok(const GemmDesc &d, int BM, int BN, int splits)
 // Largest split count <= want whose fp32 partials fit the caller's split-K workspace.
 int fit_splits(const GemmDesc &d, int want)
 {
-    int sp = want < 1 ? 1 : want;
+    int sp = want < 1 ? 1 : want;   // 0 (no request) means one
     while (sp > 1 && (!d.splitk_ws || (size_t)sp * (size_t)d.M * (size_t)d.N > d.splitk_ws_floats)) --sp;
     return sp;
+}
+
+template <typename TO, bool AK, bool BKM>
+hipError_t launch_tile(int tile, const GemmDesc &d, int splits, hipStream_t s)
+{
+    if (d.beta && splits <= 1) {   // accumulating into C: the 128x128 configurations with staged C reads
+        if (tile == 16 && d.K % 64 == 0) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4, 2, 2, true>(d, 1, s);
+        if (tile == 5 && d.K % 64 == 0) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 2, 2, 2, true>(d, 1, s);
+        if (tile == 3 || tile == 5 || tile == 16) return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2, true>(d, 1, s);
+    }
+    switch (tile) {
+    case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 2, 4>(d, splits, s);
+    case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 3, 4, 2>(d, splits, s);
+    case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 3, 2, 4>(d, splits, s);
+    case 4: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 4, 2>(d, splits, s);
+    case 5: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 2, 2, 2>(d, splits, s);
+    case 6: return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 2, 4, 2>(d, splits, s);
+    case 7: return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 2, 2, 4>(d, splits, s);
+    case 8: return launch_gemm_dl<TO, 256, 256, AK, BKM, 64, 2, 2, 4>(d, splits, s);
+    case 9: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 2, 2>(d, splits, s);
+    case 10: return launch_gemm_dl<TO, 256, 256, AK, BKM, 64, 2, 2, 2>(d, splits, s);
+    case 11: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 3, 2, 2>(d, splits, s);
+    case 12: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 3, 2, 2>(d, splits, s);
+    case 13: return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 3, 2, 4>(d, splits, s);
+    case 14: return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 3, 4, 2>(d, splits, s);
+    case 15: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 3, 2, 2>(d, splits, s);
+    case 16: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4, 2, 2>(d, splits, s);
+    case 17: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 8, 2, 2>(d, splits, s);
+    default: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, splits, s);
+    }
+}
+
+// Whether tile configuration `t` can run descriptor `d` (whole k stages,
+// whole tiles along an operand whose rows are contiguous in memory, whole
+// tiles per column block).
+bool tile_fits(const GemmDesc &d, int t)
+{
+    if (t < 0 || t >= NTILES) return false;
+    const int kd = kTileKD[t];
+    if (d.K % kd) return false;
+    if (d.N1 > 0 && (d.N1 % kTileBN[t] || d.N % kTileBN[t] || d.M % kTileBM[t])) return false;
+    if (d.N1 > 0 && (d.ylo % kd || d.yhi % kd || d.hlo % kd || d.hlen % kd)) return false;   // stages stay in one segment
+    return dl_ok(d, kTileBM[t], kTileBN[t], 1);
+}
+
+// Tuning override from the environment: "tile" or "tile,splits", in
+// LSTM355_GEMM_TILE_<class number> for one kernel class, else
+// LSTM355_GEMM_TILE for every product.
+thread_local int g_kclass = -1;
+
+bool env_choice(Choice *c)
+{
+    char name[40];
+    std::snprintf(name, sizeof(name), "LSTM355_GEMM_TILE_%d", g_kclass);
+    const char *env = std::getenv(name);
+    if (!env) env = std::getenv("LSTM355_GEMM_TILE");
+    if (!env) return false;
+    int t = std::atoi(env), sp = 0;
+    const char *comma = std::strchr(env, ',');
+    if (comma) sp = std::atoi(comma + 1);
+    if (t < 0 || t >= NTILES || sp < 0) return false;
+    *c = Choice{t, sp};
+    return true;
 }
 
 template <typename TI, typename TO, bool AK, bool BKM>
 hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
 {
     if constexpr (sizeof(TI) == 2 && !AK && !BKM) {
-        if (d.N1 > 0) {   // two column blocks: 128x128 tiles, no split
-            if (!dl_ok(d, 128, 128, 1) || d.N1 % 128) return hipErrorInvalidValue;
-            return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, 1, s);
+        if (d.N1 > 0) {   // two column blocks: no split; 128x128 tiles, 64-deep stages where they fit
+            Choice c{5, 1};
+            env_choice(&c);
+            if (!tile_fits(d, c.tile)) c.tile = 5;
+            if (!tile_fits(d, c.tile)) c.tile = 3;
+            if (!tile_fits(d, c.tile)) return hipErrorInvalidValue;
+            return launch_tile<TO, AK, BKM>(c.tile, d, 1, s);
         }
     }
     if (d.N1 > 0) return hipErrorInvalidValue;
@@ -669,23 +858,8 @@ hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
     if constexpr (sizeof(TI) == 4) {
         return launch_gemm<TI, TO, 128, 128, 64, AK, BKM>(d, c.splits, s);
     } else {
-        static const int BMs[9] = {256, 256, 128, 128, 256, 128, 256, 128, 256};
-        static const int BNs[9] = {256, 128, 256, 128, 256, 128, 128, 256, 256};
-        if (dl_ok(d, BMs[c.tile], BNs[c.tile], c.splits)) {
-            const bool k64 = d.K % 64 == 0;
-            switch (c.tile) {
-            case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 2, 4>(d, c.splits, s);
-            case 1: return launch_gemm_dl<TO, 256, 128, AK, BKM, 32, 3, 4, 2>(d, c.splits, s);
-            case 2: return launch_gemm_dl<TO, 128, 256, AK, BKM, 32, 3, 2, 4>(d, c.splits, s);
-            case 4: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 4, 2>(d, c.splits, s);
-            case 5: if (k64) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 2, 2, 2>(d, c.splits, s); break;
-            case 6: if (k64) return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 2, 4, 2>(d, c.splits, s); break;
-            case 7: if (k64) return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 2, 2, 4>(d, c.splits, s); break;
-            case 8: if (k64) return launch_gemm_dl<TO, 256, 256, AK, BKM, 64, 2, 2, 4>(d, c.splits, s); break;
-            default: break;
-            }
-            return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, c.splits, s);
-        }
+        if (tile_fits(d, c.tile)) return launch_tile<TO, AK, BKM>(c.tile, d, c.splits, s);
+        if (dl_ok(d, 128, 128, c.splits)) return launch_tile<TO, AK, BKM>(3, d, c.splits, s);
         switch (c.tile) {
         case 0: return launch_gemm<TI, TO, 256, 256, 128, AK, BKM>(d, c.splits, s);
         case 1: return launch_gemm<TI, TO, 256, 128, 128, AK, BKM>(d, c.splits, s);
@@ -735,6 +909,7 @@ hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
                 (d.out_f32 ? 4.0 : es) * (double)d.M * d.N * (d.beta ? 2.0 : 1.0);
     }
     ProfScope ps(kclass, s, flops, bytes);
+    g_kclass = kclass;
     return d.in == DType::BF16 ? dispatch_layout<bf16_t>(d, s) : dispatch_layout<float>(d, s);
 }
 

@@ -81,6 +81,20 @@ size_t colsum_partial_floats(int rows, int cols);
 hipError_t sum_rows(const float *src, int rows, int cols, float *dst, int accumulate, hipStream_t s);
 hipError_t colsum(DType t, const void *src, int rows, int cols, float *partial, float *dst, int accumulate, hipStream_t s);
 hipError_t add(DType t, size_t n, const void *a, const void *b, void *out, hipStream_t s);
+// dst[r*ldd + c] = src[r*lds + c] for r < rows, c < cols.
+hipError_t copy_rows(DType t, long rows, int cols, const void *src, long lds, void *dst, long ldd, hipStream_t s);
+// Cell update of one step for B rows x H cells (stepwise recurrence):
+// gates_t [B][4H] holds the pre-activations on entry and the activations on
+// exit; cprev [B][H] (NULL: zeros); writes c_t [B][H], m_out (storage type,
+// row stride ldm), optionally h_copy (row stride ldh) and cT.
+hipError_t gates_forward(DType t, int B, int H, float *gates_t, const float *cprev, float *c_t, void *m_out, long ldm,
+                         void *h_copy, long ldh, float *cT, int kclass, hipStream_t s);
+// Gate gradients of one step: the gradient of m_t is dm + dy + dh + dhT
+// (each may be NULL); dcn [B][H] carries dc (read, then overwritten with the
+// carry to the previous step); writes dz_t [B][4H] and, if given, dc0.
+hipError_t gates_backward(DType t, int B, int H, const float *dm, const void *dy, long ldy, const float *dh,
+                          const void *dhT, const float *gates_t, const float *c_t, const float *cprev, float *dcn,
+                          void *dz_t, float *dc0, int kclass, hipStream_t s);
 
 // Persistent recurrence kernels (recurrent.hip).
 struct RecShape {
@@ -157,6 +171,19 @@ hipError_t xcd_tripped_read_and_clear(unsigned *tripped);   // like watchdog_rea
 unsigned long long watchdog_ticks();
 hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s);
 hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &b, unsigned long long timeout, hipStream_t s);
+
+// Stepwise recurrences (stepwise.cpp): per step, the recurrent product runs
+// on the matrix-core GEMM, followed by a pointwise cell kernel (and, for
+// LSTMP, the projection product).  Used where the weights cannot stay
+// resident in a persistent kernel.
+constexpr int STEPWISE_VARIANT = 2000;   // variant reported by lstm_describe_tiling
+struct StepwiseArgs {
+    const void *R, *P;           // R [4H][Hr], P [Hp][H]
+    float *splitk_ws;            // split-K partials of the per-step products
+    size_t splitk_ws_floats;
+};
+hipError_t forward_stepwise(DType t, const RecShape &sh, const FwdBufs &b, const StepwiseArgs &w, hipStream_t s);
+hipError_t backward_stepwise(DType t, const RecShape &sh, const BwdBufs &b, const StepwiseArgs &w, hipStream_t s);
 
 // Reads (synchronously) and clears the library's sticky watchdog word on the
 // current device: nonzero if a grid barrier gave up since the last call.

@@ -74,6 +74,84 @@ __global__ __launch_bounds__(256) void add_kernel(size_t n, const T *a, const T 
         out[i] = from_f32<T>(to_f32(a[i]) + to_f32(b[i]));
 }
 
+// One step of the cell update for every (row b, cell j), after the
+// recurrent product has been added to the step's input projection:
+// z = gates_t (pre-activations in, activations i, f, g, o out, in place);
+// c_t = f c_{t-1} + i g; m_t = o tanh(c_t).
+template <typename TI>
+__global__ __launch_bounds__(256) void gates_forward_kernel(int B, int H, float *__restrict__ gates,
+                                                            const float *__restrict__ cprev, float *__restrict__ c_t,
+                                                            TI *__restrict__ m_out, long ldm, TI *__restrict__ h_copy,
+                                                            long ldh, float *__restrict__ cT)
+{
+    const long n = (long)B * H;
+    for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+        const int b = (int)(e / H), j = (int)(e % H);
+        float *g = gates + (long)b * 4 * H + j;
+        const float ig = sigmoid_f(g[0]), fg = sigmoid_f(g[H]), gg = tanh_f(g[2 * H]), og = sigmoid_f(g[3 * H]);
+        const float cp = cprev ? cprev[e] : 0.0f;
+        const float c = fg * cp + ig * gg;
+        const TI m = from_f32<TI>(og * tanh_f(c));
+        g[0] = ig;
+        g[H] = fg;
+        g[2 * H] = gg;
+        g[3 * H] = og;
+        c_t[e] = c;
+        m_out[(long)b * ldm + j] = m;
+        if (h_copy) h_copy[(long)b * ldh + j] = m;
+        if (cT) cT[e] = c;
+    }
+}
+
+// Gate gradients of one step for every (row b, cell j).  The gradient of
+// m_t is the sum of the given terms: dm (fp32), dy (storage type, row
+// stride ldy), dh (fp32) and dhT (storage type).  dcn carries the cell
+// gradient between steps (in: from step t+1, out: to step t-1).
+template <typename TI>
+__global__ __launch_bounds__(256) void gates_backward_kernel(int B, int H, const float *__restrict__ dm_in,
+                                                             const TI *__restrict__ dy, long ldy,
+                                                             const float *__restrict__ dh_in, const TI *__restrict__ dhT,
+                                                             const float *__restrict__ gates, const float *__restrict__ c_t,
+                                                             const float *__restrict__ cprev, float *__restrict__ dcn,
+                                                             TI *__restrict__ dz, float *__restrict__ dc0)
+{
+    const long n = (long)B * H;
+    for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+        const int b = (int)(e / H), j = (int)(e % H);
+        float dm = 0.0f;
+        if (dm_in) dm += dm_in[e];
+        if (dy) dm += to_f32(dy[(long)b * ldy + j]);
+        if (dh_in) dm += dh_in[e];
+        if (dhT) dm += to_f32(dhT[e]);
+        const float *g = gates + (long)b * 4 * H + j;
+        const float ig = g[0], fg = g[H], gg = g[2 * H], og = g[3 * H];
+        const float tc = tanh_f(c_t[e]);
+        const float d_o = dm * tc;
+        const float d_c = dcn[e] + dm * og * (1.0f - tc * tc);
+        const float cp = cprev ? cprev[e] : 0.0f;
+        const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cp;
+        TI *z = dz + (long)b * 4 * H + j;
+        z[0] = from_f32<TI>(d_i * ig * (1.0f - ig));
+        z[H] = from_f32<TI>(d_f * fg * (1.0f - fg));
+        z[2 * H] = from_f32<TI>(d_g * (1.0f - gg * gg));
+        z[3 * H] = from_f32<TI>(d_o * og * (1.0f - og));
+        const float nc = d_c * fg;
+        dcn[e] = nc;
+        if (dc0) dc0[e] = nc;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void copy_rows_kernel(long rows, int cols, const T *__restrict__ src, long lds,
+                                                        T *__restrict__ dst, long ldd)
+{
+    const long n = rows * cols;
+    for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+        const long r = e / cols, c = e % cols;
+        dst[r * ldd + c] = src[r * lds + c];
+    }
+}
+
 int grid_for(size_t n)
 {
     size_t g = (n + 255) / 256;
@@ -134,6 +212,52 @@ hipError_t sum_rows(const float *src, int rows, int cols, float *dst, int accumu
 {
     ProfScope ps(K_SMALL, s, 0.0, (double)rows * cols * 4.0);
     hipLaunchKernelGGL(colsum_pass2, dim3((cols + 255) / 256), dim3(256), 0, s, src, rows, cols, dst, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t gates_forward(DType t, int B, int H, float *gates_t, const float *cprev, float *c_t, void *m_out, long ldm,
+                         void *h_copy, long ldh, float *cT, int kclass, hipStream_t s)
+{
+    const double n = (double)B * H;
+    ProfScope ps(kclass, s, 0.0, n * (4.0 * 4 * 2 + 4.0 * (cprev ? 2 : 1) + dsize(t) * (h_copy ? 2 : 1)));
+    const size_t ne = (size_t)B * H;
+    if (t == DType::BF16)
+        hipLaunchKernelGGL(gates_forward_kernel<bf16_t>, dim3(grid_for(ne)), dim3(256), 0, s, B, H, gates_t, cprev, c_t,
+                           static_cast<bf16_t *>(m_out), ldm, static_cast<bf16_t *>(h_copy), ldh, cT);
+    else
+        hipLaunchKernelGGL(gates_forward_kernel<float>, dim3(grid_for(ne)), dim3(256), 0, s, B, H, gates_t, cprev, c_t,
+                           static_cast<float *>(m_out), ldm, static_cast<float *>(h_copy), ldh, cT);
+    return hipGetLastError();
+}
+
+hipError_t gates_backward(DType t, int B, int H, const float *dm, const void *dy, long ldy, const float *dh,
+                          const void *dhT, const float *gates_t, const float *c_t, const float *cprev, float *dcn,
+                          void *dz_t, float *dc0, int kclass, hipStream_t s)
+{
+    const double n = (double)B * H;
+    ProfScope ps(kclass, s, 0.0, n * (4.0 * 4 + 4.0 * 4 + dsize(t) * 4));
+    const size_t ne = (size_t)B * H;
+    if (t == DType::BF16)
+        hipLaunchKernelGGL(gates_backward_kernel<bf16_t>, dim3(grid_for(ne)), dim3(256), 0, s, B, H, dm,
+                           static_cast<const bf16_t *>(dy), ldy, dh, static_cast<const bf16_t *>(dhT), gates_t, c_t,
+                           cprev, dcn, static_cast<bf16_t *>(dz_t), dc0);
+    else
+        hipLaunchKernelGGL(gates_backward_kernel<float>, dim3(grid_for(ne)), dim3(256), 0, s, B, H, dm,
+                           static_cast<const float *>(dy), ldy, dh, static_cast<const float *>(dhT), gates_t, c_t,
+                           cprev, dcn, static_cast<float *>(dz_t), dc0);
+    return hipGetLastError();
+}
+
+hipError_t copy_rows(DType t, long rows, int cols, const void *src, long lds, void *dst, long ldd, hipStream_t s)
+{
+    ProfScope ps(K_SMALL, s, 0.0, 2.0 * rows * cols * dsize(t));
+    const size_t ne = (size_t)rows * cols;
+    if (t == DType::BF16)
+        hipLaunchKernelGGL(copy_rows_kernel<bf16_t>, dim3(grid_for(ne)), dim3(256), 0, s, rows, cols,
+                           static_cast<const bf16_t *>(src), lds, static_cast<bf16_t *>(dst), ldd);
+    else
+        hipLaunchKernelGGL(copy_rows_kernel<float>, dim3(grid_for(ne)), dim3(256), 0, s, rows, cols,
+                           static_cast<const float *>(src), lds, static_cast<float *>(dst), ldd);
     return hipGetLastError();
 }
 

@@ -143,6 +143,33 @@ def test_layer_parity(T, B, I, H, Hp, dtype, reverse):
         assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
+STEPWISE_VARIANT = 2000
+
+STEPWISE_CASES = [
+    # (T, B, I, H, Hp, dtype, reverse, states): the per-step GEMM sequence
+    (6, 19, 24, 48, 16, "f32", False, True),      # LSTMP, ragged everything
+    (5, 33, 48, 136, 40, "bf16", True, True),     # LSTMP reverse
+    (4, 64, 128, 256, 128, "bf16", False, False), # LSTMP on whole tiles, no initial state
+    (5, 37, 40, 72, 0, "f32", False, True),       # plain LSTM
+    (3, 130, 64, 96, 0, "bf16", True, True),      # plain LSTM reverse, two row tiles
+    (1, 9, 16, 32, 8, "bf16", False, True),       # a single step
+]
+
+
+@pytest.mark.parametrize("T,B,I,H,Hp,dtype,reverse,states", STEPWISE_CASES)
+def test_stepwise_recurrence_parity(T, B, I, H, Hp, dtype, reverse, states, monkeypatch):
+    """The stepwise recurrence (per-step GEMMs and cell kernels), forced on
+    shapes the persistent kernels would otherwise take."""
+    monkeypatch.setenv("LSTM355_RECURRENCE", "stepwise")
+    label = f"stepwise T{T} B{B} I{I} H{H} Hp{Hp} {dtype} rev{int(reverse)} states{int(states)}"
+    announce(label)
+    c = layer_case(T, B, I, H, Hp, dtype, reverse, seed=T * 100 + B + 7, states=states, final_grads=states)
+    gpu = run_layer_gpu(c, T, B, I, H, Hp, dtype, reverse)
+    ref = oracle_layer(c, Hp, reverse)
+    check_layer(gpu, ref, dtype, label)
+    assert gpu["tiling"][3] == STEPWISE_VARIANT, gpu["tiling"]
+
+
 def test_layer_without_initial_state_or_final_grads():
     T, B, I, H = 6, 9, 32, 40
     announce("layer zero states")
