@@ -209,15 +209,6 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
         char *wv = static_cast<char *>(workspace);
         float *gates = reinterpret_cast<float *>(rv + h->r_gates);
 
-        GemmDesc g{};
-        g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
-        g.M = (int)h->TB; g.N = (int)h->G4; g.K = d.I;
-        g.A = x; g.lda = h->ldx;
-        g.B = W; g.ldb = d.I;
-        g.C = gates; g.ldc = h->G4;
-        g.bias = b; g.beta = 0;
-        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
-
         RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, h->ldy};
         FwdBufs fb{};
         fb.R = R; fb.P = P; fb.h0 = h0; fb.c0 = c0;
@@ -227,11 +218,22 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
         fb.y = y; fb.hT = hT; fb.cT = cT;
         fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
         const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+
+        GemmDesc g{};
+        g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
+        g.M = (int)h->TB; g.N = (int)h->G4; g.K = d.I;
+        g.A = x; g.lda = h->ldx;
+        g.B = W; g.ldb = d.I;
+        g.C = gates; g.ldc = h->G4;
+        g.bias = b; g.beta = 0;
+        if (xcd) g.side = xcd_prep_forward(sh, fb);   // the recurrence's exchange rows and flags
+        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+
         if (!xcd && use_stepwise(h, h->fwd_ok)) {
             StepwiseArgs sw{R, P, reinterpret_cast<float *>(wv + h->w_split), h->split_floats};
             TRY_HIP("forward recurrence (stepwise)", forward_stepwise(h->dt, sh, fb, sw, s));
         } else if (xcd) {
-            TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s));
+            TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s, true));
         } else {
             TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
         }
@@ -277,10 +279,6 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         RecShape sh{T, B, I, H, Hp, d.reverse, h->ldy};
         const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
         const bool stepwise = !xcd && use_stepwise(h, h->bwd_ok);
-        if (!stepwise) {   // the persistent kernels keep rows of R^T (and P^T)
-            TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s));
-            if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
-        }
 
         BwdBufs bb{};
         bb.Rt = Rt; bb.Pt = Pt; bb.dy = dy; bb.dhT = dhT; bb.dcT = dcT; bb.h0 = h0; bb.c0 = c0;
@@ -292,11 +290,16 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         bb.dh0 = dh0; bb.dc0 = dc0;
         bb.dbpart = reinterpret_cast<float *>(wv + h->w_part);
         bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
+        if (!stepwise) {   // the persistent kernels keep rows of R^T (and P^T)
+            const SideJob prep = xcd ? xcd_prep_backward(sh, bb) : SideJob{};
+            TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s, xcd ? &prep : nullptr));
+            if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));
+        }
         if (stepwise) {
             StepwiseArgs sw{R, P, split_ws, h->split_floats};
             TRY_HIP("backward recurrence (stepwise)", backward_stepwise(h->dt, sh, bb, sw, s));
         } else if (xcd) {
-            TRY_HIP("backward recurrence (XCD-local)", launch_backward_xcd(sh, bb, watchdog_ticks(), s));
+            TRY_HIP("backward recurrence (XCD-local)", launch_backward_xcd(sh, bb, watchdog_ticks(), s, true));
         } else {
             TRY_HIP("backward recurrence", launch_backward(h->dt, sh, h->bwd, bb, s));
         }
@@ -326,6 +329,13 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             }
             g.hlen = B;
             g.C2 = dR; g.ldc2 = Hr;
+            if (xcd) {   // db = sum of the recurrence's per-XCD partials, done by the same launch
+                g.side.sum_src = reinterpret_cast<const float *>(wv + h->w_part);
+                g.side.sum_rows = 8;
+                g.side.sum_cols = (int)G4;
+                g.side.sum_dst = db;
+                g.side.sum_acc = accumulate;
+            }
             if (gemm_dual_ok(g)) {
                 TRY_HIP("dW|dR", gemm(g, s, K_GEMM_DWR));
                 fused = true;
@@ -371,9 +381,10 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             }
             if (!beta) TRY_HIP("dR zero", fill_u32(dR, (size_t)G4 * Hr, 0u, s));
         }
-        if (xcd)   // the recurrence left one fp32 partial per XCD
-            TRY_HIP("db", sum_rows(reinterpret_cast<const float *>(wv + h->w_part), 8, (int)G4, db, accumulate, s));
-        else
+        if (xcd) {   // the recurrence left one fp32 partial per XCD (the fused product sums them itself)
+            if (!fused)
+                TRY_HIP("db", sum_rows(reinterpret_cast<const float *>(wv + h->w_part), 8, (int)G4, db, accumulate, s));
+        } else
             TRY_HIP("db", colsum(h->dt, dz, (int)TB, (int)G4, reinterpret_cast<float *>(wv + h->w_part), db, accumulate, s));
         if (Hp) {  // dP = sum_t dh_t^T m_t
             GemmDesc g{};

@@ -18,6 +18,7 @@
 // result does not depend on scheduling.
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "side_job.hpp"
 
 #include <cstdio>
 #include <cstdlib>
@@ -44,6 +45,7 @@ struct GemmArgs {
     int ylo, yhi, yoff, hlo, hlen;
     char *C2;
     long ldc2;
+    SideJob side;
 };
 
 // Global -> register -> LDS staging of one operand for one K stage.
@@ -145,7 +147,10 @@ __global__ __launch_bounds__(256, (BM * BN > 128 * 128) ? 1 : 2) void gemm_kerne
     // each XCD a contiguous run of tiles (shared operand rows stay in its L2).
     const int bid = blockIdx.x;
     const int tile = (bid & 7) * g.per_xcd + (bid >> 3);
-    if (tile >= g.ntiles) return;
+    if (tile >= g.ntiles) {
+        run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+        return;
+    }
     const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = blockIdx.y * g.kchunk;
@@ -231,6 +236,7 @@ __global__ __launch_bounds__(256, (BM * BN > 128 * 128) ? 1 : 2) void gemm_kerne
                 }
             }
         }
+    run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
 }
 
 // ---------------------------------------------------------------------------
@@ -362,7 +368,10 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 
     const int bid = blockIdx.x;
     const int tile = (bid & 7) * g.per_xcd + (bid >> 3);
-    if (tile >= g.ntiles) return;
+    if (tile >= g.ntiles) {
+        run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+        return;
+    }
     const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
     // second column block: its own B operand segments, k range and output
@@ -497,6 +506,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
                 }
             }
         }
+    run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
 }
 
 // C[m][n] = (beta ? C : 0) + bias[n] + sum over splits of partial[s][m][n], in split order.
@@ -593,6 +603,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.B3 = static_cast<const char *>(d.B3); g.ldb3 = d.ldb3; g.b3_bytes = d.b3_bytes;
     g.ylo = d.ylo; g.yhi = d.yhi; g.yoff = d.yoff; g.hlo = d.hlo; g.hlen = d.hlen;
     g.C2 = static_cast<char *>(d.C2); g.ldc2 = d.ldc2;
+    g.side = d.side;
     auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN, CB>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
@@ -622,6 +633,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
     g.N1 = 0; g.B2 = g.B3 = nullptr; g.C2 = nullptr;
+    g.side = d.side;
     auto kern = gemm_kernel<TI, TO, BM, BN, KB, AK, BKM>;
     if (LDS > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),

@@ -36,6 +36,26 @@ struct ProfScope {
     void *ev0;
 };
 
+// Work a launch can take on beside its own, spread over all of its
+// workgroups once they have finished their own work (so that the extra
+// stores do not delay the waits of its main loop): fill rows of 16-bit
+// elements with a value, clear 32-bit words, and sum the rows of a small
+// fp32 matrix into a vector (deterministic, in row order).  It saves the
+// separate launches of these bandwidth-trivial steps.
+struct SideJob {
+    uint16_t *fill = nullptr;   // fill[r*fill_ld + c] = fill_v, r < fill_rows, c < fill_cols
+    long fill_rows = 0;
+    int fill_cols = 0;
+    long fill_ld = 0;
+    uint16_t fill_v = 0;
+    unsigned *clr = nullptr;    // clr[i] = 0, i < clr_n
+    int clr_n = 0;
+    const float *sum_src = nullptr;   // sum_dst[c] (+)= sum_{r < sum_rows} sum_src[r*sum_cols + c]
+    int sum_rows = 0, sum_cols = 0;
+    float *sum_dst = nullptr;
+    int sum_acc = 0;
+};
+
 // C[m][n] (beta ? C : 0) + sum_k A(m,k) B(n,k) (+ bias[n])
 //   A(m,k) = a_kmajor ? A[m*lda + k] : A[k*lda + m]
 //   B(n,k) = b_kmajor ? B[n*ldb + k] : B[k*ldb + n]
@@ -64,13 +84,16 @@ struct GemmDesc {
     const void *B3 = nullptr; long ldb3 = 0; long b3_bytes = 0;
     int ylo = 0, yhi = 0, yoff = 0, hlo = 0, hlen = 0;
     void *C2 = nullptr; long ldc2 = 0;
+    SideJob side;              // done by the product's workgroups after their tiles
 };
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
 // Whether a descriptor with a second column block (N1 > 0) can run.
 bool gemm_dual_ok(const GemmDesc &d);
 
 // Small kernels.
-hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s);  // dst[c][r] = src[r][c]
+// dst[c][r] = src[r][c]; `side` (optional) is done by the same launch.
+hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s,
+                     const SideJob *side = nullptr);
 hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
 // p[r*ld + c] = v for r < rows, c < cols (16-bit elements).
 hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s);
@@ -169,8 +192,18 @@ constexpr int XCD_VARIANT = 1000;   // variant reported by lstm_describe_tiling 
 void xcd_path_disable();
 hipError_t xcd_tripped_read_and_clear(unsigned *tripped);   // like watchdog_read_and_clear
 unsigned long long watchdog_ticks();
-hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s);
-hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &b, unsigned long long timeout, hipStream_t s);
+// The exchanged rows (y forward, dz backward) must hold XCD_NOT_READY and the
+// XCD_WORDS words at XCD_FLAGS of the sync block must be zero when these
+// kernels start: the launch functions prepare both unless `prepared` says an
+// earlier launch on the stream (xcd_prep_forward / xcd_prep_backward as a
+// side job) already did.
+constexpr uint16_t XCD_NOT_READY = 0xffffu;
+SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
+SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);
+hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s,
+                              bool prepared = false);
+hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &b, unsigned long long timeout, hipStream_t s,
+                               bool prepared = false);
 
 // Stepwise recurrences (stepwise.cpp): per step, the recurrent product runs
 // on the matrix-core GEMM, followed by a pointwise cell kernel (and, for

@@ -3,6 +3,7 @@
 // stack composition adds, and word fills for barrier counters.
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "side_job.hpp"
 
 namespace lstm355 {
 
@@ -10,7 +11,8 @@ namespace {
 
 // 64x64 tiles through LDS; both the read and the write are row-contiguous.
 template <typename T>
-__global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ src, int rows, int cols, T *__restrict__ dst)
+__global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ src, int rows, int cols, T *__restrict__ dst,
+                                                        SideJob side)
 {
     __shared__ T tile[64][65];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
@@ -20,6 +22,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ sr
     __syncthreads();
     for (int i = ty; i < 64; i += 4)
         if (c0 + i < cols && r0 + tx < rows) dst[(long)(c0 + i) * rows + r0 + tx] = tile[tx][i];
+    run_side_job(side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
 }
 
 __global__ void fill_kernel(uint32_t *p, size_t n, uint32_t v)
@@ -161,16 +164,17 @@ int grid_for(size_t n)
 
 }  // namespace
 
-hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s)
+hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s, const SideJob *side)
 {
     ProfScope ps(K_SMALL, s, 0.0, 2.0 * rows * (double)cols * dsize(t));
     dim3 grid((cols + 63) / 64, (rows + 63) / 64);
+    const SideJob sj = side ? *side : SideJob{};
     if (t == DType::BF16)
         hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t *>(src), rows,
-                           cols, static_cast<bf16_t *>(dst));
+                           cols, static_cast<bf16_t *>(dst), sj);
     else
         hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, static_cast<const float *>(src), rows, cols,
-                           static_cast<float *>(dst));
+                           static_cast<float *>(dst), sj);
     return hipGetLastError();
 }
 

@@ -110,7 +110,7 @@ __device__ __forceinline__ void wait_own_lds() { asm volatile("s_waitcnt lgkmcnt
 // element is written exactly once, never with that pattern (a NaN of that
 // encoding is replaced by the canonical quiet NaN).  A consumer therefore
 // knows an element is final once it reads anything else.
-constexpr bf16_t NOT_READY = 0xffffu;
+constexpr bf16_t NOT_READY = XCD_NOT_READY;
 
 __device__ __forceinline__ bf16_t ready_value(bf16_t v) { return v == NOT_READY ? (bf16_t)0x7fc0u : v; }
 
@@ -522,7 +522,34 @@ int mbx_for(int B)
 }
 }  // namespace
 
-hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned long long timeout, hipStream_t s)
+SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &bf)
+{
+    SideJob j;
+    j.clr = bf.sync + XCD_FLAGS;
+    j.clr_n = XCD_WORDS;
+    j.fill = static_cast<uint16_t *>(bf.y);   // the kernel's consumers wait for these elements to change
+    j.fill_rows = (long)sh.T * sh.B;
+    j.fill_cols = sh.H;
+    j.fill_ld = sh.ldy;
+    j.fill_v = NOT_READY;
+    return j;
+}
+
+SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &bf)
+{
+    SideJob j;
+    j.clr = bf.sync + XCD_FLAGS;
+    j.clr_n = XCD_WORDS;
+    j.fill = static_cast<uint16_t *>(bf.dz);
+    j.fill_rows = (long)sh.T * sh.B;
+    j.fill_cols = 4 * sh.H;
+    j.fill_ld = 4L * sh.H;
+    j.fill_v = NOT_READY;
+    return j;
+}
+
+hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned long long timeout, hipStream_t s,
+                              bool prepared)
 {
     XFwdArgs a;
     a.T = sh.T; a.B = sh.B; a.H = sh.H; a.reverse = sh.reverse; a.RX = (sh.B + NXCD - 1) / NXCD; a.ldy = sh.ldy;
@@ -534,11 +561,13 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     a.cT = bf.cT;
     a.flags = bf.sync + XCD_FLAGS;
     a.timeout = timeout;
-    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
-    if (e != hipSuccess) return e;
-    // the kernel's consumers wait for these elements to change
-    e = fill_rows_u16(bf.y, (long)sh.T * sh.B, sh.H, sh.ldy, NOT_READY, s);
-    if (e != hipSuccess) return e;
+    if (!prepared) {
+        hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+        if (e != hipSuccess) return e;
+        // the kernel's consumers wait for these elements to change
+        e = fill_rows_u16(bf.y, (long)sh.T * sh.B, sh.H, sh.ldy, NOT_READY, s);
+        if (e != hipSuccess) return e;
+    }
     const double G4 = 4.0 * sh.H;
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
                  (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0);
@@ -552,7 +581,8 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned long long timeout, hipStream_t s)
+hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned long long timeout, hipStream_t s,
+                               bool prepared)
 {
     XBwdArgs a;
     a.T = sh.T; a.B = sh.B; a.H = sh.H; a.reverse = sh.reverse; a.RX = (sh.B + NXCD - 1) / NXCD; a.ldy = sh.ldy;
@@ -566,11 +596,13 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
     a.dbpart = bf.dbpart;
     a.flags = bf.sync + XCD_FLAGS;
     a.timeout = timeout;
-    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
-    if (e != hipSuccess) return e;
-    // the kernel's consumers wait for these elements to change
-    e = fill_rows_u16(bf.dz, (long)sh.T * sh.B, 4 * sh.H, 4L * sh.H, NOT_READY, s);
-    if (e != hipSuccess) return e;
+    if (!prepared) {
+        hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+        if (e != hipSuccess) return e;
+        // the kernel's consumers wait for these elements to change
+        e = fill_rows_u16(bf.dz, (long)sh.T * sh.B, 4 * sh.H, 4L * sh.H, NOT_READY, s);
+        if (e != hipSuccess) return e;
+    }
     const double G4 = 4.0 * sh.H;
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
                  (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0);
