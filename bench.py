@@ -88,6 +88,65 @@ def cpu_baseline(wl, rows: int):
                       f"forward + backward, fp64; {dt:.1f} s wall"}
 
 
+# Kernel classes whose launches are one kernel each, by kernel-name prefix
+# (for attributing the per-dispatch counter values to a class).
+CLASS_KERNELS = {"recurrent_fwd": "lstm_fwd_xcd", "recurrent_bwd": "lstm_bwd_xcd"}
+
+
+def _short_kernel(name: str) -> str:
+    import re
+    name = name.replace("lstm355::(anonymous namespace)::", "").replace("void ", "")
+    return re.sub(r"\(.*$", "", name)
+
+
+def _counter_avgs(path: str):
+    """Per kernel name: (dispatches, average counter value) of a rocprofv3
+    counter-collection CSV holding one counter."""
+    import collections
+    import csv
+    agg = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            agg[_short_kernel(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return {k: (len(v), sum(v) / len(v)) for k, v in agg.items()}
+
+
+def traffic_from(pmc_dir: str, workload: str, copy_mib: int):
+    """Writes profiles/traffic.json from four rocprofv3 --pmc runs under
+    pmc_dir: fetch/ and write/ (FETCH_SIZE, WRITE_SIZE of the benchmark
+    step) and cfetch/ and cwrite/ (the same counters for a plain copy of
+    copy_mib MiB, which fixes the scale of each counter: KiB counted per KiB
+    actually moved)."""
+    def one(sub):
+        import glob
+        files = glob.glob(os.path.join(pmc_dir, sub, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {os.path.join(pmc_dir, sub)}")
+        return _counter_avgs(files[0])
+    fetch, write, cfetch, cwrite = one("fetch"), one("write"), one("cfetch"), one("cwrite")
+    copy_kib = copy_mib * 1024.0
+    cf = [v for k, (n, v) in cfetch.items() if "copyBuffer" in k]
+    cw = [v for k, (n, v) in cwrite.items() if "copyBuffer" in k]
+    fetch_factor = copy_kib / max(cf)
+    write_factor = copy_kib / max(cw)
+    by_name = {}
+    for k in fetch:
+        if k in write:
+            by_name[k] = (fetch[k][1] * fetch_factor + write[k][1] * write_factor) * 1024.0
+    kernels = {}
+    for cls, prefix in CLASS_KERNELS.items():
+        hits = [v for k, v in by_name.items() if k.startswith(prefix)]
+        if len(hits) == 1:
+            kernels[cls] = {"hbm_bytes_per_launch": hits[0]}
+    out = {"source_hash": kernel_source_hash(), "workload": workload, "fetch_factor": fetch_factor,
+           "write_factor": write_factor, "copy_bytes": copy_mib * (1 << 20),
+           "kernels": kernels, "bytes_per_dispatch_by_kernel": by_name}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    print(json.dumps({"traffic_file": TRAFFIC_FILE, "kernels": kernels, "fetch_factor": fetch_factor,
+                      "write_factor": write_factor}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -99,7 +158,15 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain torch copy of this many MiB (counter calibration) and exit")
+    ap.add_argument("--traffic-from", default="",
+                    help="write profiles/traffic.json from rocprofv3 --pmc runs in this directory and exit "
+                         "(no GPU needed)")
     args = ap.parse_args()
+
+    if args.traffic_from:
+        import synth  # noqa: F401
+        traffic_from(args.traffic_from, workload_name(make_workload(args)), 256)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
