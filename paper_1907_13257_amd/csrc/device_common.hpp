@@ -33,9 +33,11 @@ template <> __device__ __forceinline__ float from_f32<float>(float v) { return v
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
 // Gate non-linearities in fp32.  sigma(u) = 1/(1+e^-u); tanh(u) = 2 sigma(2u) - 1.
-// Both saturate correctly: e^-u overflows to +inf for very negative u, giving 0.
-__device__ __forceinline__ float sigmoid_f(float u) { return 1.0f / (1.0f + __expf(-u)); }
-__device__ __forceinline__ float tanh_f(float u) { return 2.0f / (1.0f + __expf(-2.0f * u)) - 1.0f; }
+// The reciprocal is the hardware's (v_rcp_f32, within 1 ulp) rather than an
+// IEEE division sequence.  Both saturate correctly: e^-u overflows to +inf
+// for very negative u, and rcp(+inf) = 0.
+__device__ __forceinline__ float sigmoid_f(float u) { return __builtin_amdgcn_rcpf(1.0f + __expf(-u)); }
+__device__ __forceinline__ float tanh_f(float u) { return 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u)) - 1.0f; }
 
 // ---------------------------------------------------------------------------
 // MFMA wrappers.  A "fragment" is the 16 bytes one lane contributes per

@@ -123,12 +123,13 @@ __device__ __forceinline__ bool any_not_ready(u32x4 v)
 }
 
 // acc[i] = (16 exchanged rows, this wave's k range) x rf[i] on the matrix
-// cores, once every element of the first `valid` rows is final.  Each attempt
+// cores (WT: the transposed product, rf[i] x the rows), once every element of
+// the first `valid` rows is final.  Each attempt
 // copies the wave's slice from the XCD's L2 into its LDS tile (L1 bypassed)
 // and multiplies it while checking for NOT_READY; an attempt that saw one is
 // discarded and repeated.  Returns false if another workgroup aborted or the
 // wall-clock watchdog expired (then the abort word is raised).
-template <int RB, int KCW, int NBX>
+template <int RB, int KCW, int NBX, bool WT = false>
 __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld, int kbyte, unsigned tile,
                                                      const char *tilep, int lane, int valid,
                                                      const u32x4 (&rf)[NBX][KCW], f32x4 (&acc)[NBX],
@@ -152,7 +153,12 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
             const u32x4 fa = stage_frag<RB>(tilep, c, lane);
             late |= any_not_ready(fa);
 #pragma unroll
-            for (int i = 0; i < NBX; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
+            for (int i = 0; i < NBX; ++i) {
+                if (WT)
+                    mfma16(acc[i], rf[i][c], fa, bf16_t{});
+                else
+                    mfma16(acc[i], fa, rf[i][c], bf16_t{});
+            }
         }
         const unsigned long long lm = __builtin_amdgcn_ballot_w64(late && row_in);
         if (lm == 0) return true;
@@ -188,7 +194,11 @@ struct XFwdArgs {
 
 // Wave w multiplies the k range [w*H/8, (w+1)*H/8) for all 4*HN gate rows of
 // the workgroup's cells; the eight partial sums meet in LDS.  MBX blocks of
-// 16 batch rows per XCD.
+// 16 batch rows per XCD.  The resident gate rows are ordered cell-major
+// (row 4u + g is gate g of cell u) and the product is taken transposed
+// (gate rows x batch rows), so each lane ends with the four gates of one
+// cell for one batch row: one 16-byte LDS store per block, and the gate math
+// reads each wave's partial sums of a cell with one 16-byte load.
 template <int HN, int MBX>
 __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 {
@@ -199,7 +209,7 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
     constexpr int RB = KW * 2;        // staged bytes per row
     constexpr int NCELL = 16 * HN;    // cells of one row block
     constexpr int RP = NT + 36;       // padded partial-sum row (conflict-free writes, few read conflicts)
-    __shared__ float red[8][16][RP];
+    __shared__ __attribute__((aligned(16))) float red[8][16][RP];
     __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
     __shared__ int s_ok;
 
@@ -213,12 +223,13 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 
     if (!placed_ok(a.flags, &s_ok)) return;
 
-    // resident weights: the 4*HN rows of R feeding this workgroup's cells, this wave's k range
+    // resident weights: the 4*HN rows of R feeding this workgroup's cells
+    // (cell-major: row 4u + g), this wave's k range
     u32x4 rf[NB][KCW];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         const int n = i * 16 + (lane & 15);
-        const int g = n / HN, u = n % HN;
+        const int g = n & 3, u = n >> 2;
         const bf16_t *rrow = a.R + (long)(g * H + j0 + u) * H + w * KW;
 #pragma unroll
         for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + c * 32 + (lane >> 4) * 8);
@@ -260,8 +271,8 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
             const int rb0 = row0 + mb * 16;
             if (mb > 0) wait_own_lds();   // the previous block's fragment reads are done
             if (s > 0) {
-                if (!stage_mma_when_ready<RB, KCW, NB>(rs_y, (long)tprev * B + rb0, a.ldy, w * KW * 2, tile, stage[w],
-                                                       lane, rowend - rb0, rf, acc, a.flags, a.timeout))
+                if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_y, (long)tprev * B + rb0, a.ldy, w * KW * 2, tile,
+                                                             stage[w], lane, rowend - rb0, rf, acc, a.flags, a.timeout))
                     s_bad = 1;
             } else if (a.h0) {
                 stage_rows<RB>(rs_h0, rb0, H, w * KW * 2, tile, lane);
@@ -270,24 +281,23 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                 for (int c = 0; c < KCW; ++c) {
                     const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
 #pragma unroll
-                    for (int i = 0; i < NB; ++i) mfma16(acc[i], fa, rf[i][c], bf16_t{});
+                    for (int i = 0; i < NB; ++i) mfma16(acc[i], rf[i][c], fa, bf16_t{});
                 }
             }
+            // lane: batch row lane%16, gates 0..3 of cell 4i + lane/16 of block i
 #pragma unroll
             for (int i = 0; i < NB; ++i)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+                *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
             __syncthreads();
             if (s_bad) return;   // the same decision in every wave
             const int b = rb0 + cr;
             if (has_cell && b < rowend) {
-                float z[4];
+                float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    float v = gx[mb][g];
+                for (int q = 0; q < 8; ++q) {
+                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][cr][4 * cu]);
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) v += red[q][cr][g * HN + cu];
-                    z[g] = v;
+                    for (int g = 0; g < 4; ++g) z[g] += p[g];
                 }
                 const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
                 const float c = fg * creg[mb] + ig * gg;
