@@ -114,13 +114,19 @@ constexpr bf16_t NOT_READY = XCD_NOT_READY;
 
 __device__ __forceinline__ bf16_t ready_value(bf16_t v) { return v == NOT_READY ? (bf16_t)0x7fc0u : v; }
 
-__device__ __forceinline__ bool any_not_ready(u32x4 v)
+// Running per-half maximum of the bf16 patterns a lane has read: NOT_READY
+// (0xffff) is the largest 16-bit value, so a lane read one exactly when a
+// half of its maximum is 0xffff.  Four packed max operations per fragment.
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ u16x2 max_halves(u16x2 m, u32x4 v)
 {
-    bool r = false;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) r |= (v[e] & 0xffffu) == 0xffffu || (v[e] >> 16) == 0xffffu;
-    return r;
+    const u16x2 a = __builtin_elementwise_max(__builtin_bit_cast(u16x2, v[0]), __builtin_bit_cast(u16x2, v[1]));
+    const u16x2 b = __builtin_elementwise_max(__builtin_bit_cast(u16x2, v[2]), __builtin_bit_cast(u16x2, v[3]));
+    return __builtin_elementwise_max(m, __builtin_elementwise_max(a, b));
 }
+
+__device__ __forceinline__ bool saw_not_ready(u16x2 m) { return m.x == NOT_READY || m.y == NOT_READY; }
 
 // acc[i] = (16 exchanged rows, this wave's k range) x rf[i] on the matrix
 // cores (WT: the transposed product, rf[i] x the rows), once every element of
@@ -147,11 +153,13 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
         wait_own_loads();
 #pragma unroll
         for (int i = 0; i < NBX; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        bool late = false;
+        u16x2 seen = {0, 0};
 #pragma unroll
         for (int c = 0; c < KCW; ++c) {
+            // fragments in flight at most four chunks ahead (bounded registers)
+            if (c % 4 == 0 && c > 0) __builtin_amdgcn_sched_barrier(0);
             const u32x4 fa = stage_frag<RB>(tilep, c, lane);
-            late |= any_not_ready(fa);
+            seen = max_halves(seen, fa);
 #pragma unroll
             for (int i = 0; i < NBX; ++i) {
                 if (WT)
@@ -160,7 +168,7 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
                     mfma16(acc[i], fa, rf[i][c], bf16_t{});
             }
         }
-        const unsigned long long lm = __builtin_amdgcn_ballot_w64(late && row_in);
+        const unsigned long long lm = __builtin_amdgcn_ballot_w64(saw_not_ready(seen) && row_in);
         if (lm == 0) return true;
         // re-copy only the instructions that cover rows still incomplete
         const unsigned rows = (unsigned)(lm | (lm >> 16) | (lm >> 32) | (lm >> 48)) & 0xffffu;
