@@ -18,15 +18,9 @@ typedef uint16_t bf16_t;
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float(((unsigned)v) << 16); }
 
-// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ bf16_t f32_to_bf16(float f)
-{
-    unsigned u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u)
-        return (bf16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
-}
+// fp32 -> bf16, round to nearest even; NaN stays a NaN.  gfx950 converts in
+// one instruction (v_cvt_pk_bf16_f32, rounding per the default RNE mode).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 template <typename TI> __device__ __forceinline__ TI from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
