@@ -146,7 +146,12 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
     const __amdgpu_buffer_rsrc_t rfl = rsrc(flags);
     const bool row_in = (lane & 15) < valid;
     const unsigned long long t0 = wall_clock64();
-    unsigned qmask = ~0u;
+    // copy only the instructions that cover valid rows (an XCD may own fewer
+    // than 16 rows); the other rows of the tile feed only discarded outputs
+    unsigned qmask = 0;
+#pragma unroll
+    for (int q = 0; q < 16 / RPI; ++q)
+        if (q * RPI < valid) qmask |= 1u << q;
     while (true) {
         stage_rows<RB, true>(rs, r0, ld, kbyte, tile, lane, qmask);
         const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
