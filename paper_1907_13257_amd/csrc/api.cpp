@@ -414,7 +414,7 @@ extern "C" lstm_status_t lstm_check(lstm_handle_t h, void *workspace, void *stre
         // workgroups were not spread over the XCDs as the XCD-local kernels
         // require: stop using them in this process
         xcd_path_disable();
-        std::snprintf(g_detail, sizeof(g_detail), "XCD-local kernel found a workgroup on an unexpected XCD; "
+        std::snprintf(g_detail, sizeof(g_detail), "XCD-local kernel did not get one workgroup per (XCD, slot); "
                                                   "falling back to the generic kernels from now on");
         return LSTM_ERR_UNSUPPORTED;
     }

@@ -177,12 +177,13 @@ constexpr size_t SYNC_BYTES = 4096;
 constexpr int SYNC_COUNT0 = 0;     // barrier counter of the generic kernels
 constexpr int SYNC_ABORT = 64;     // abort flag of the generic kernels
 constexpr int SYNC_WORDS = 128;    // words cleared before a generic launch
-constexpr int XCD_FLAGS = 256;     // per-workgroup step counters of the XCD-local kernels (256 words)
+constexpr int XCD_FLAGS = 256;     // words of the XCD-local kernels (257 words)
+constexpr int XCD_CLAIM = 0;       // 8 per-XCD masks of claimed workgroup slots, relative to XCD_FLAGS
 constexpr int XCD_ABORT = 256;     // abort flag, relative to XCD_FLAGS
 constexpr int XCD_WORDS = 257;     // words cleared before an XCD-local launch
 
 // Sticky error bits of the library (device variable): 1 = a watchdog expired,
-// 2 = an XCD-local kernel found a workgroup on an unexpected XCD.
+// 2 = an XCD-local launch did not give every (XCD, slot) role exactly one workgroup.
 constexpr unsigned TRIP_WATCHDOG = 1u, TRIP_PLACEMENT = 2u;
 
 // XCD-local recurrences (recurrent_xcd.hip): bf16, plain LSTM, H in {256,

@@ -2,8 +2,8 @@
 // exchange stays inside one XCD (bf16, plain LSTM, H in {256, 512, 1024}).
 //
 // The MI355X has 8 XCDs of 32 CUs, each XCD with its own L2; a 256-workgroup
-// launch places workgroup w on XCD w % 8 (checked at run time against the
-// XCC_ID register).  XCD x owns batch rows [x*RX, x*RX + RX), RX = ceil(B/8),
+// launch puts 32 workgroups on each XCD, and a workgroup takes the XCD it
+// finds itself on (XCC_ID register) as its own.  XCD x owns batch rows [x*RX, x*RX + RX), RX = ceil(B/8),
 // and all H cells of those rows: its 32 workgroups each own HN = H/32 cells.
 // The rows of h_{t-1} (forward) and of dz_t (backward) that a workgroup needs
 // are therefore produced inside its own XCD and travel through that XCD's
@@ -41,20 +41,30 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p)
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, 0x7fffffff, 0x00020000);
 }
 
-// Placement check: this workgroup must run on XCD blockIdx.x % 8.
-__device__ __forceinline__ bool placed_ok(unsigned *flags, int *s_ok)
+// Role of a workgroup: its XCD is the one it runs on (XCC_ID register) and
+// its slot within the XCD is blockIdx.x / 8.  Dispatch hands workgroups to
+// the XCDs in turn, so the XCD of workgroup w is (w + o) % 8 for an offset o
+// that depends on earlier dispatches; the 32 workgroups of an XCD then have
+// distinct slots.  Each workgroup claims its slot in a per-XCD bit mask; a
+// slot claimed twice means the roles do not cover every (XCD, slot) pair, and
+// the launch is abandoned (abort word set, placement error recorded).
+__device__ __forceinline__ bool claim_role(unsigned *flags, int *s_xcd)
 {
     if (threadIdx.x == 0) {
-        const unsigned x = __builtin_amdgcn_s_getreg(HWREG_XCC_ID) & 0xfu;
-        int ok = x == (blockIdx.x & 7u);
-        if (!ok) {
+        const int x = (int)(__builtin_amdgcn_s_getreg(HWREG_XCC_ID) & 7u);
+        const unsigned bit = 1u << (blockIdx.x >> 3);
+        const unsigned prev =
+            __hip_atomic_fetch_or(flags + XCD_CLAIM + x, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev & bit) {
             __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_PLACEMENT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            *s_xcd = -1;
+        } else {
+            *s_xcd = x;
         }
-        *s_ok = ok;
     }
     __syncthreads();
-    return *s_ok != 0;
+    return *s_xcd >= 0;
 }
 
 // Staging of exchanged rows.  Each wave copies the rows it multiplies (16
@@ -224,17 +234,16 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
     constexpr int RP = NT + 36;       // padded partial-sum row (conflict-free writes, few read conflicts)
     __shared__ __attribute__((aligned(16))) float red[8][16][RP];
     __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
-    __shared__ int s_ok;
+    __shared__ int s_xcd;
 
+    if (!claim_role(a.flags, &s_xcd)) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int xcd = s_xcd, slot = blockIdx.x >> 3;
     const int H = a.H, B = a.B;
     const long G4 = 4L * H;
     const int j0 = slot * HN;
     const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
     const unsigned tile = lds_addr(&stage[w][0]);
-
-    if (!placed_ok(a.flags, &s_ok)) return;
 
     // resident weights: the 4*HN rows of R feeding this workgroup's cells
     // (cell-major: row 4u + g), this wave's k range
@@ -366,17 +375,16 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
     constexpr int RP = NC + 4;                    // padded partial-sum row (conflict-free writes)
     __shared__ float red[8][16][RP];
     __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
-    __shared__ int s_ok;
+    __shared__ int s_xcd;
 
+    if (!claim_role(a.flags, &s_xcd)) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int xcd = s_xcd, slot = blockIdx.x >> 3;
     const int H = a.H, B = a.B;
     const long G4 = 4L * H;
     const int j0 = slot * HN;
     const int row0 = xcd * a.RX, rowend = min(B, row0 + a.RX);
     const unsigned tile = lds_addr(&stage[w][0]);
-
-    if (!placed_ok(a.flags, &s_ok)) return;
 
     // resident weights: rows of R^T (= columns of R) of the owned cells, this wave's k range
     u32x4 rf[NBB][KCW];
@@ -501,12 +509,38 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
     }
 }
 
-template <typename K>
-hipError_t coop512(K kernel, hipStream_t s, void *argp)
+// Launch of 256 workgroups, one per CU.  The kernels need every workgroup of
+// an XCD resident at once (consumers wait for producers).  Kernels small
+// enough for two workgroups per CU reserve unused LDS so that a CU holds one,
+// and on an otherwise idle device a plain dispatch then makes all 256
+// resident.  A plain dispatch avoids the queue synchronisation that a
+// cooperative launch adds before and after the kernel (about 11 us each).
+// Roles are checked in the kernel and every wait has a watchdog, so a launch
+// that does not get its workgroups as expected ends every wave and
+// lstm_check reports it.
+constexpr int ONE_PER_CU_LDS = 96 * 1024;   // more than half of a CU's 160 KiB
+
+template <auto kernel>
+hipError_t launch256(hipStream_t s, void *argp)
 {
+    struct Cfg {
+        unsigned dyn;
+        int per_cu;
+    };
+    static const Cfg cfg = [] {
+        Cfg c{0u, 0};
+        hipFuncAttributes fa;
+        if (hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel)) != hipSuccess) return c;
+        if (fa.sharedSizeBytes < (size_t)ONE_PER_CU_LDS) c.dyn = (unsigned)(ONE_PER_CU_LDS - fa.sharedSizeBytes);
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&c.per_cu, reinterpret_cast<const void *>(kernel), XT,
+                                                         c.dyn) != hipSuccess)
+            c.per_cu = 0;
+        return c;
+    }();
+    if (cfg.per_cu != 1) return hipErrorCooperativeLaunchTooLarge;
     void *args[] = {argp};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(kernel), dim3(NXCD * WG_PER_XCD), dim3(XT), args,
-                                      0u, s);
+    return hipLaunchKernel(reinterpret_cast<const void *>(kernel), dim3(NXCD * WG_PER_XCD), dim3(XT), args, cfg.dyn,
+                           s);
 }
 
 int g_xcd_disabled = 0;
@@ -596,7 +630,7 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
                  (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
 #define FWD_CASE(HN_, M_) \
-    if (sh.H == 32 * HN_ && m == M_) return coop512(lstm_fwd_xcd<HN_, M_>, s, &a);
+    if (sh.H == 32 * HN_ && m == M_) return launch256<lstm_fwd_xcd<HN_, M_>>(s, &a);
     FWD_CASE(8, 1) FWD_CASE(8, 2) FWD_CASE(8, 4)
     FWD_CASE(16, 1) FWD_CASE(16, 2) FWD_CASE(16, 4)
     FWD_CASE(32, 1) FWD_CASE(32, 2) FWD_CASE(32, 4)
@@ -631,7 +665,7 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
                  (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
 #define BWD_CASE(HN_, M_) \
-    if (sh.H == 32 * HN_ && m == M_) return coop512(lstm_bwd_xcd<HN_, M_>, s, &a);
+    if (sh.H == 32 * HN_ && m == M_) return launch256<lstm_bwd_xcd<HN_, M_>>(s, &a);
     BWD_CASE(8, 1) BWD_CASE(8, 2) BWD_CASE(8, 4)
     BWD_CASE(16, 1) BWD_CASE(16, 2) BWD_CASE(16, 4)
     BWD_CASE(32, 1) BWD_CASE(32, 2) BWD_CASE(32, 4)
