@@ -661,16 +661,23 @@ struct Choice {
 //   9: 256x256, 2x2, 32, 4     10: 256x256, 2x2, 64, 2   11: 128x256, 2x2, 32, 3
 //  12: 256x128, 2x2, 32, 3     13: 128x256, 2x4, 64, 3   14: 256x128, 4x2, 64, 3
 //  15: 128x128, 2x2, 64, 3     16: 128x128, 2x2, 64, 4   17: 128x128, 2x2, 32, 8
+//  18: 64x128, 2x2, 64, 3       19: 64x64, 2x2, 64, 4     20: 128x64, 2x2, 64, 3
 // (16 and 17 keep 96 / 112 KiB of operands in flight per workgroup: the
-// per-step recurrent products stream their weights from HBM once)
-constexpr int NTILES = 18;
-const int kTileBM[NTILES] = {256, 256, 128, 128, 256, 128, 256, 128, 256, 256, 256, 128, 256, 128, 256, 128, 128, 128};
-const int kTileBN[NTILES] = {256, 128, 256, 128, 256, 128, 128, 256, 256, 256, 256, 256, 128, 256, 128, 128, 128, 128};
-const int kTileKD[NTILES] = {32, 32, 32, 32, 32, 64, 64, 64, 64, 32, 64, 32, 32, 64, 64, 64, 64, 32};
+// per-step recurrent products stream their weights from HBM once; 18-20
+// give the skinny per-step products more workgroups.  An operand whose rows
+// are the contiguous dimension needs 128 of them per tile: its LDS swizzle
+// spans 16 chunks of 16 bytes.)
+constexpr int NTILES = 21;
+const int kTileBM[NTILES] = {256, 256, 128, 128, 256, 128, 256, 128, 256, 256, 256,
+                             128, 256, 128, 256, 128, 128, 128, 64,  64,  128};
+const int kTileBN[NTILES] = {256, 128, 256, 128, 256, 128, 128, 256, 256, 256, 256,
+                             256, 128, 256, 128, 128, 128, 128, 128, 64,  64};
+const int kTileKD[NTILES] = {32, 32, 32, 32, 32, 64, 64, 64, 64, 32, 64, 32, 32, 64, 64, 64, 64, 32, 64, 64, 64};
 // Workgroups of each configuration that fit on one CU (LDS-limited).
-const int kTileSlots[NTILES] = {1, 1, 1, 2, 1, 2, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, 1};
+const int kTileSlots[NTILES] = {1, 1, 1, 2, 1, 2, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, 1, 2, 2, 2};
 
 bool dl_ok(const GemmDesc &d, int BM, int BN, int splits);
+bool tile_fits(const GemmDesc &d, int t);
 bool env_choice(Choice *c);
 
 // Split count for tile shape BM x BN with `slots` workgroups per CU: enough
@@ -710,7 +717,23 @@ Choice choose(const GemmDesc &d, size_t es)
     }
     if (es == 2 && d.M <= 256 && d.K % 64 == 0 && dl_ok(d, 128, 128, 1)) {
         // skinny products (one step of the stepwise recurrence) stream their
-        // weight operand once: deep rings keep enough of it in flight
+        // weight operand once.  Measured on the wide LSTMP layer's per-step
+        // shapes (M = 128): accumulating with a k-contiguous weight, 128x64
+        // tiles (512 workgroups at N = 32768) beat 128x128 by 17%; a long-K
+        // product with both operands k-contiguous runs best on 64x64 tiles
+        // split to about 256 workgroups (30%); an M-major weight with many
+        // output columns on unsplit 64x128 tiles (25%); otherwise the deep
+        // 128x128 ring, split along K to fill the CUs.
+        const long rows64 = (d.M + 63) / 64;
+        if (d.beta && d.b_kmajor && (long)((d.N + 63) / 64) * ((d.M + 127) / 128) >= 256 && tile_fits(d, 20))
+            return Choice{20, 1};
+        if (d.a_kmajor && d.b_kmajor && tile_fits(d, 19)) {
+            const long tiles = rows64 * ((d.N + 63) / 64);
+            int sp = 1;
+            while (sp < 64 && tiles * sp < 256 && d.K / (2 * sp) >= 256) sp *= 2;
+            if (sp == 1 || !d.beta) return Choice{19, sp};
+        }
+        if (d.a_kmajor && !d.b_kmajor && rows64 * (d.N / 128) >= 128 && tile_fits(d, 18)) return Choice{18, 1};
         return Choice{16, model_splits(d, 128, 128, 1, 64)};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
@@ -795,6 +818,10 @@ hipError_t launch_tile(int tile, const GemmDesc &d, int splits, hipStream_t s)
         if (tile == 16 && d.K % 64 == 0) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4, 2, 2, true>(d, 1, s);
         if (tile == 5 && d.K % 64 == 0) return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 2, 2, 2, true>(d, 1, s);
         if (tile == 3 || tile == 5 || tile == 16) return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2, true>(d, 1, s);
+        if constexpr (AK && BKM) {
+            if (tile == 19 && d.K % 64 == 0) return launch_gemm_dl<TO, 64, 64, AK, BKM, 64, 4, 2, 2, true>(d, 1, s);
+            if (tile == 20 && d.K % 64 == 0) return launch_gemm_dl<TO, 128, 64, AK, BKM, 64, 3, 2, 2, true>(d, 1, s);
+        }
     }
     switch (tile) {
     case 0: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 2, 4>(d, splits, s);
@@ -814,6 +841,15 @@ hipError_t launch_tile(int tile, const GemmDesc &d, int splits, hipStream_t s)
     case 15: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 3, 2, 2>(d, splits, s);
     case 16: return launch_gemm_dl<TO, 128, 128, AK, BKM, 64, 4, 2, 2>(d, splits, s);
     case 17: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 8, 2, 2>(d, splits, s);
+    case 18:
+        if constexpr (AK) return launch_gemm_dl<TO, 64, 128, AK, BKM, 64, 3, 2, 2>(d, splits, s);
+        return hipErrorInvalidValue;
+    case 19:
+        if constexpr (AK && BKM) return launch_gemm_dl<TO, 64, 64, AK, BKM, 64, 4, 2, 2>(d, splits, s);
+        return hipErrorInvalidValue;
+    case 20:
+        if constexpr (BKM) return launch_gemm_dl<TO, 128, 64, AK, BKM, 64, 3, 2, 2>(d, splits, s);
+        return hipErrorInvalidValue;
     default: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, splits, s);
     }
 }
@@ -826,6 +862,7 @@ bool tile_fits(const GemmDesc &d, int t)
     if (t < 0 || t >= NTILES) return false;
     const int kd = kTileKD[t];
     if (d.K % kd) return false;
+    if ((!d.a_kmajor && kTileBM[t] < 128) || (!d.b_kmajor && kTileBN[t] < 128)) return false;
     if (d.N1 > 0 && (d.N1 % kTileBN[t] || d.N % kTileBN[t] || d.M % kTileBM[t])) return false;
     if (d.N1 > 0 && (d.ylo % kd || d.yhi % kd || d.hlo % kd || d.hlen % kd)) return false;   // stages stay in one segment
     return dl_ok(d, kTileBM[t], kTileBN[t], 1);
