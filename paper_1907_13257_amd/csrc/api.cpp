@@ -163,7 +163,7 @@ extern "C" lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out
             if (pf < (size_t)8 * G4) pf = (size_t)8 * G4;   // per-XCD bias partials
             h->w_part = o; o = align256(o + pf * 4);
         }
-        // split-K partials of the weight-gradient products (up to 4 splits)
+        // split-K partials of the weight- and input-gradient products
         {
             size_t mn = (size_t)G4 * (size_t)(d.I > Hr ? d.I : Hr);
             if (d.Hp && (size_t)d.Hp * d.H > mn) mn = (size_t)d.Hp * d.H;
@@ -309,6 +309,8 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
             g.in = h->dt; g.out_f32 = h->dt == DType::F32; g.a_kmajor = true; g.b_kmajor = false;
             g.M = (int)TB; g.N = I; g.K = (int)G4;
             g.A = dz; g.lda = G4; g.B = W; g.ldb = I; g.C = dx; g.ldc = h->ldx;
+            // few output tiles over a long K (small batches, wide layers): split K
+            g.splitk_ws = split_ws; g.splitk_ws_floats = h->split_floats;
             TRY_HIP("dx", gemm(g, s, K_GEMM_DX));
         }
         // [dW | dR] = dZ^T [X | H_prev] as one product when the shapes allow
