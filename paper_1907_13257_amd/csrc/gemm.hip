@@ -46,6 +46,12 @@ struct GemmArgs {
     char *C2;
     long ldc2;
     SideJob side;
+    // fused cell update (see GemmDesc)
+    int cell_h;
+    const float *cell_prev;
+    float *cell_c, *cell_cT;
+    bf16_t *cell_m;
+    long cell_ldm;
 };
 
 // Global -> register -> LDS staging of one operand for one K stage.
@@ -281,6 +287,8 @@ struct DmaOperand {
     u32x4 rsrc;                                   // buffer descriptor (base, limit, format)
     long ld;                                      // elements
     int r0;
+    int ilv = 0;                                  // > 0 (K-major only): tile row n reads memory row
+                                                  // (n % 4) * ilv + n / 4 (cell-major gate order)
 
     __device__ __forceinline__ void init(const char *base, long ld_, int r0_, long bound_bytes)
     {
@@ -299,7 +307,9 @@ struct DmaOperand {
             if (KMAJ) {
                 const int row = byte / L::RB, p = (byte % L::RB) >> 4;
                 const int c = L::kslot(row, p);   // the swizzle is an involution
-                off = (unsigned)((((long)(r0 + row) * ld + k0) << 1) + c * 16);
+                const int n = r0 + row;
+                const long mrow = ilv ? (long)(n & 3) * ilv + (n >> 2) : (long)n;
+                off = (unsigned)(((mrow * ld + k0) << 1) + c * 16);
             } else {
                 const int k = byte / L::RP, p = (byte % L::RP) >> 4;
                 const int c = L::mslot(k, p);
@@ -353,9 +363,14 @@ __device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int 
 
 // NWM x NWN waves; wave (wm, wn) owns the (BM/NWM) x (BN/NWN) block of the tile.
 // CB: the instantiation used when C is accumulated into (beta = 1, no split).
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false>
+// GT: fused cell update (GemmDesc::cell_h): tile columns are cell-major gates
+// (column n is gate n % 4 of cell n / 4), and the epilogue applies the cell
+// equations to the four gates of each (row, cell) through LDS.
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false,
+          bool GT = false>
 __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 {
+    static_assert(!GT || (CB && BKM && BN % 4 == 0), "the cell update accumulates onto C with a k-major B");
     constexpr int NW = NWM * NWN;
     constexpr int WM = BM / NWM, WN = BN / NWN;
     constexpr int FM = WM / 32, FN = WN / 32;
@@ -395,6 +410,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)g.K * g.lda * 2);
     if (!second) {
         db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
+        if (GT) db.ilv = g.cell_h;
     } else {
         db.init(g.B2, g.ldb2, n0 - g.N1, g.b2_bytes);
         dh.init(g.B3 ? g.B3 : g.B2, g.ldb3, n0 - g.N1, g.B3 ? g.b3_bytes : 0);
@@ -456,6 +472,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     TO *cbase = reinterpret_cast<TO *>(second ? g.C2 : g.C);
     const long ldc = second ? g.ldc2 : g.ldc;
     const int coff = second ? g.N1 : 0;
+    // column of C (the gate pre-activations) that tile column `col` holds
+    auto ccol = [&](int col) -> long { return GT ? (long)(col & 3) * g.cell_h + (col >> 2) : (long)(col - coff); };
     // beta, CB instantiations: C is read block by block before anything is
     // stored (a load may not pass an earlier store to C in program order, so
     // interleaving them would expose one memory latency per element).  The
@@ -475,7 +493,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                        cv[j][v] = (row < g.M && col < g.N) ? to_f32(cbase[(long)row * ldc + (col - coff)]) : 0.0f;
+                        cv[j][v] = (row < g.M && col < g.N) ? to_f32(cbase[(long)row * ldc + ccol(col)]) : 0.0f;
                     }
                 }
 #pragma unroll
@@ -483,6 +501,47 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) acc[i][j0 + j][v] += cv[j][v];
             }
+    }
+    if constexpr (GT) {
+        // z of the tile into LDS (the operand stages are no longer read), then
+        // one (row, cell) pair per thread and pass: the four gates of a cell
+        // are adjacent columns
+        constexpr int ZP = BN + 4;
+        static_assert(BM * ZP * 4 <= NS * STAGE, "the z tile fits in the operand stages");
+        float *zt = reinterpret_cast<float *>(smem);
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int r = wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                    zt[r * ZP + wn * WN + j * 32 + (lane & 31)] = acc[i][j][v];
+                }
+        __syncthreads();
+        constexpr int CELLS = BN / 4;
+        const int H = g.cell_h;
+        for (int p = tid; p < BM * CELLS; p += 64 * NW) {
+            const int r = p / CELLS, u = p % CELLS;
+            const int row = m0 + r, cell = n0 / 4 + u;
+            if (row >= g.M || cell >= H) continue;
+            const f32x4 z = *reinterpret_cast<const f32x4 *>(&zt[r * ZP + 4 * u]);
+            const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+            const long e = (long)row * H + cell;
+            const float cp = g.cell_prev ? g.cell_prev[e] : 0.0f;
+            const float c = fg * cp + ig * gg;
+            float *gp = reinterpret_cast<float *>(cbase) + (long)row * ldc + cell;
+            gp[0] = ig;
+            gp[H] = fg;
+            gp[2 * H] = gg;
+            gp[3 * H] = og;
+            g.cell_c[e] = c;
+            g.cell_m[(long)row * g.cell_ldm + cell] = f32_to_bf16(og * tanh_f(c));
+            if (g.cell_cT) g.cell_cT[e] = c;
+        }
+        run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+        return;
     }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -581,7 +640,8 @@ hipError_t launch_splitk_reduce(const GemmDesc &d, int splits, hipStream_t s)
     return hipGetLastError();
 }
 
-template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false>
+template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false,
+          bool GT = false>
 hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
 {
     constexpr int LDS = NS * (BM + BN) * KD * 2;
@@ -604,7 +664,10 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.ylo = d.ylo; g.yhi = d.yhi; g.yoff = d.yoff; g.hlo = d.hlo; g.hlen = d.hlen;
     g.C2 = static_cast<char *>(d.C2); g.ldc2 = d.ldc2;
     g.side = d.side;
-    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN, CB>;
+    g.cell_h = GT ? d.cell_h : 0;
+    g.cell_prev = d.cell_prev; g.cell_c = d.cell_c; g.cell_cT = d.cell_cT;
+    g.cell_m = static_cast<bf16_t *>(d.cell_m); g.cell_ldm = d.cell_ldm;
+    auto kern = gemm_dl_kernel<TO, BM, BN, AK, BKM, KD, NS, NWM, NWN, CB, GT>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (e != hipSuccess) return e;
@@ -942,6 +1005,13 @@ bool gemm_dual_ok(const GemmDesc &d)
     return dl_ok(d, 128, 128, 1);
 }
 
+bool gemm_cell_ok(const GemmDesc &d)
+{
+    if (d.cell_h <= 0 || d.in != DType::BF16 || !d.a_kmajor || !d.b_kmajor || !d.out_f32 || !d.beta) return false;
+    if (d.N1 > 0 || d.bias || !d.cell_c || !d.cell_m || d.N != 4 * d.cell_h || d.cell_h % 16 || d.K % 64) return false;
+    return dl_ok(d, 128, 64, 1);
+}
+
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
 {
     if (d.M <= 0 || d.N <= 0 || d.K <= 0) return hipSuccess;
@@ -957,8 +1027,13 @@ hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
         bytes = es * ((double)d.M * d.K + (double)d.N * d.K) +
                 (d.out_f32 ? 4.0 : es) * (double)d.M * d.N * (d.beta ? 2.0 : 1.0);
     }
+    if (d.cell_h > 0) {   // the cell update's own traffic: read cprev, write activations, c, m
+        if (!gemm_cell_ok(d)) return hipErrorInvalidValue;
+        bytes += (double)d.M * d.cell_h * (4.0 * (d.cell_prev ? 1 : 0) + 4.0 + 2.0 + (d.cell_cT ? 4.0 : 0.0));
+    }
     ProfScope ps(kclass, s, flops, bytes);
     g_kclass = kclass;
+    if (d.cell_h > 0) return launch_gemm_dl<float, 128, 64, true, true, 64, 3, 2, 2, true, true>(d, 1, s);
     return d.in == DType::BF16 ? dispatch_layout<bf16_t>(d, s) : dispatch_layout<float>(d, s);
 }
 

@@ -85,7 +85,20 @@ struct GemmDesc {
     int ylo = 0, yhi = 0, yoff = 0, hlo = 0, hlen = 0;
     void *C2 = nullptr; long ldc2 = 0;
     SideJob side;              // done by the product's workgroups after their tiles
+    // Optional fused LSTM cell update (bf16 operands, both k-major, fp32 C
+    // accumulated into, N = 4 * cell_h): C holds the gate pre-activations of
+    // H = cell_h cells in row blocks (i, f, g, o).  Instead of storing z, the
+    // product stores the activations into C, c = f*cprev + i*g into cell_c,
+    // m = o*tanh(c) (bf16) into cell_m[row*cell_ldm + j] and, if non-NULL,
+    // c into cell_cT.  cell_prev NULL means a zero previous cell state.
+    int cell_h = 0;
+    const float *cell_prev = nullptr;
+    float *cell_c = nullptr;
+    void *cell_m = nullptr; long cell_ldm = 0;
+    float *cell_cT = nullptr;
 };
+// Whether `gemm` can run the fused cell update for descriptor d.
+bool gemm_cell_ok(const GemmDesc &d);
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
 // Whether a descriptor with a second column block (N1 > 0) can run.
 bool gemm_dual_ok(const GemmDesc &d);

@@ -7,6 +7,7 @@
 //   gates_t += h_{t'} R^T        matrix-core GEMM, accumulated onto the input
 //                                projection already stored in gates_t
 //   cell update                  pointwise: activations in place, c_t, m_t
+//                                (LSTMP in bf16: in the GEMM's epilogue)
 //   h_t = P m_t (LSTMP)          GEMM (split over k), written into y_t
 // Backward, steps in reverse visiting order:
 //   dm = P^T dh_t (LSTMP)        GEMM; dh_t = dy_t + P-side carry, kept in dH
@@ -53,6 +54,11 @@ hipError_t forward_stepwise(DType t, const RecShape &sh, const FwdBufs &b, const
         const bool last = st == T - 1;
         float *gates_t = b.gates + (long)tt * B * G4;
         const void *hprev = st > 0 ? static_cast<const void *>(y + (long)tprev * B * sh.ldy * es) : b.h0;
+        const float *cprev = st > 0 ? b.cs + (long)tprev * B * H : b.c0;
+        float *c_t = b.cs + (long)tt * B * H;
+        char *y_t = y + (long)tt * B * sh.ldy * es;
+        char *m_t = Hp ? static_cast<char *>(b.ms) + (long)tt * B * H * es : nullptr;
+        bool cell_done = false;
         if (hprev) {   // z_t = Gx_t + h_{t'} R^T
             GemmDesc g = base_desc(t, w);
             g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
@@ -60,14 +66,21 @@ hipError_t forward_stepwise(DType t, const RecShape &sh, const FwdBufs &b, const
             g.A = hprev; g.lda = st > 0 ? sh.ldy : Hr;
             g.B = w.R; g.ldb = Hr;
             g.C = gates_t; g.ldc = G4; g.beta = 1;
-            RET_IF(gemm(g, s, K_REC_FWD));
+            if (Hp) {   // the cell update in the product's epilogue when it fits
+                GemmDesc f = g;
+                f.cell_h = H; f.cell_prev = cprev; f.cell_c = c_t; f.cell_m = m_t; f.cell_ldm = H;
+                f.cell_cT = last ? b.cT : nullptr;
+                if (gemm_cell_ok(f)) {
+                    RET_IF(gemm(f, s, K_REC_FWD));
+                    cell_done = true;
+                }
+            }
+            if (!cell_done) RET_IF(gemm(g, s, K_REC_FWD));
         }
-        const float *cprev = st > 0 ? b.cs + (long)tprev * B * H : b.c0;
-        float *c_t = b.cs + (long)tt * B * H;
-        char *y_t = y + (long)tt * B * sh.ldy * es;
         if (Hp) {
-            char *m_t = static_cast<char *>(b.ms) + (long)tt * B * H * es;
-            RET_IF(gates_forward(t, B, H, gates_t, cprev, c_t, m_t, H, nullptr, 0, last ? b.cT : nullptr, K_REC_FWD, s));
+            if (!cell_done)
+                RET_IF(gates_forward(t, B, H, gates_t, cprev, c_t, m_t, H, nullptr, 0, last ? b.cT : nullptr, K_REC_FWD,
+                                     s));
             GemmDesc g = base_desc(t, w);   // h_t = P m_t
             g.out_f32 = t == DType::F32; g.a_kmajor = true; g.b_kmajor = true;
             g.M = B; g.N = Hp; g.K = H;

@@ -150,6 +150,7 @@ STEPWISE_CASES = [
     (6, 19, 24, 48, 16, "f32", False, True),      # LSTMP, ragged everything
     (5, 33, 48, 136, 40, "bf16", True, True),     # LSTMP reverse
     (4, 64, 128, 256, 128, "bf16", False, False), # LSTMP on whole tiles, no initial state
+    (4, 130, 64, 128, 64, "bf16", True, True),    # LSTMP, cell update in the product: two row tiles, states
     (5, 37, 40, 72, 0, "f32", False, True),       # plain LSTM
     (3, 130, 64, 96, 0, "bf16", True, True),      # plain LSTM reverse, two row tiles
     (1, 9, 16, 32, 8, "bf16", False, True),       # a single step
