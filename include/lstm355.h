@@ -111,6 +111,15 @@ lstm_status_t lstm_backward(lstm_handle_t h,
                             float *dW, float *dR, float *db, float *dP,
                             int accumulate, void *workspace, void *stream);
 
+/* Environment: LSTM355_XCD_LAUNCH=cooperative makes the persistent
+ * recurrence kernels of the bf16 path wait, as cooperative launches, until
+ * all their workgroups (one per CU) can be resident.  By default they are
+ * plain dispatches, which saves about 11 us of queue synchronisation per
+ * launch but relies on the device not running other kernels beside them;
+ * if it does, their waits time out and lstm_check reports LSTM_ERR_TIMEOUT.
+ * Use the cooperative launch when other streams (for example collectives
+ * overlapping the backward pass) share the device. */
+
 /* Synchronises `stream` and reports whether any kernel of the library gave up
  * at a grid barrier on the current device since the last check
  * (LSTM_ERR_TIMEOUT; the device-wide flag is then cleared).  Outputs of such a

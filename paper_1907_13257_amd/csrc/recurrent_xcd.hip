@@ -21,6 +21,9 @@
 // producers, and a consumer proceeds as soon as the values it uses are
 // there.  Every wait has a wall-clock watchdog and an abort word, so every
 // wave exits.
+#include <cstdlib>
+#include <cstring>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -517,8 +520,17 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 // cooperative launch adds before and after the kernel (about 11 us each).
 // Roles are checked in the kernel and every wait has a watchdog, so a launch
 // that does not get its workgroups as expected ends every wave and
-// lstm_check reports it.
+// lstm_check reports it.  When other kernels may occupy CUs at the same time
+// (another stream, collectives overlapping the backward pass),
+// LSTM355_XCD_LAUNCH=cooperative selects a cooperative launch, which waits
+// until all 256 workgroups can be resident.
 constexpr int ONE_PER_CU_LDS = 96 * 1024;   // more than half of a CU's 160 KiB
+
+bool cooperative_requested()
+{
+    const char *env = std::getenv("LSTM355_XCD_LAUNCH");
+    return env && std::strcmp(env, "cooperative") == 0;
+}
 
 template <auto kernel>
 hipError_t launch256(hipStream_t s, void *argp)
@@ -539,8 +551,10 @@ hipError_t launch256(hipStream_t s, void *argp)
     }();
     if (cfg.per_cu != 1) return hipErrorCooperativeLaunchTooLarge;
     void *args[] = {argp};
-    return hipLaunchKernel(reinterpret_cast<const void *>(kernel), dim3(NXCD * WG_PER_XCD), dim3(XT), args, cfg.dyn,
-                           s);
+    const void *f = reinterpret_cast<const void *>(kernel);
+    if (cooperative_requested())
+        return hipLaunchCooperativeKernel(f, dim3(NXCD * WG_PER_XCD), dim3(XT), args, cfg.dyn, s);
+    return hipLaunchKernel(f, dim3(NXCD * WG_PER_XCD), dim3(XT), args, cfg.dyn, s);
 }
 
 int g_xcd_disabled = 0;

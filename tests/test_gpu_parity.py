@@ -143,6 +143,25 @@ def test_layer_parity(T, B, I, H, Hp, dtype, reverse):
         assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
+@pytest.mark.parametrize("T,B,I,H,reverse", [(6, 40, 64, 256, False), (4, 130, 32, 1024, True)])
+def test_xcd_cooperative_launch_parity(T, B, I, H, reverse, monkeypatch):
+    """The XCD-local recurrences launched cooperatively (the mode for devices
+    shared with other streams) give the same results as the plain dispatch."""
+    monkeypatch.setenv("LSTM355_XCD_LAUNCH", "cooperative")
+    label = f"cooperative T{T} B{B} I{I} H{H} rev{int(reverse)}"
+    announce(label)
+    c = layer_case(T, B, I, H, 0, "bf16", reverse, seed=T * 1000 + B + 3)
+    gpu = run_layer_gpu(c, T, B, I, H, 0, "bf16", reverse)
+    check_layer(gpu, oracle_layer(c, 0, reverse), "bf16", label)
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert gpu["tiling"][3] == XCD_VARIANT, gpu["tiling"]
+    monkeypatch.delenv("LSTM355_XCD_LAUNCH")
+    plain = run_layer_gpu(c, T, B, I, H, 0, "bf16", reverse)
+    for k in gpu:
+        if k != "tiling" and gpu[k] is not None:
+            assert np.array_equal(gpu[k], plain[k]), k   # same kernels, same order of arithmetic
+
+
 STEPWISE_VARIANT = 2000
 
 STEPWISE_CASES = [
