@@ -398,7 +398,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
         kbeg = g.ylo;
         kend = g.yhi;
     }
-    const int nst = (kend - kbeg) / KD;
+    // a last partial stage only when both operands are m-major: its rows past
+    // K lie beyond the operands' buffer bounds and load as zeros
+    const int nst = (kend - kbeg + KD - 1) / KD;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -856,7 +858,7 @@ bool dl_ok(const GemmDesc &d, int BM, int BN, int splits)
 {
     const char *env = std::getenv("LSTM355_GEMM_DL");
     if (env && env[0] == '0') return false;
-    if (d.K % 32) return false;
+    if (d.K % 32 && (d.a_kmajor || d.b_kmajor)) return false;   // a partial last stage needs k as the row index
     if (!d.a_kmajor && d.M % BM) return false;
     if (!d.b_kmajor && d.N % BN) return false;
     const long ea = d.a_kmajor ? (long)d.M * d.lda : (long)d.K * d.lda;
@@ -924,7 +926,7 @@ bool tile_fits(const GemmDesc &d, int t)
 {
     if (t < 0 || t >= NTILES) return false;
     const int kd = kTileKD[t];
-    if (d.K % kd) return false;
+    if (d.K % kd && (d.a_kmajor || d.b_kmajor)) return false;
     if ((!d.a_kmajor && kTileBM[t] < 128) || (!d.b_kmajor && kTileBN[t] < 128)) return false;
     if (d.N1 > 0 && (d.N1 % kTileBN[t] || d.N % kTileBN[t] || d.M % kTileBM[t])) return false;
     if (d.N1 > 0 && (d.ylo % kd || d.yhi % kd || d.hlo % kd || d.hlen % kd)) return false;   // stages stay in one segment
