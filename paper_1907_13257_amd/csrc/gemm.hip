@@ -20,6 +20,7 @@
 #include "kernels.hpp"
 #include "side_job.hpp"
 
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -36,6 +37,7 @@ struct GemmArgs {
     const float *bias;
     int beta;
     int tiles_n, ntiles, per_xcd;
+    int band;                    // tile columns per band of the tile order (tiles_n: row-major)
     int kchunk;                  // K per split (multiple of the stage depth)
     float *partial;              // split > 1: fp32 partials [split][M][N]
     // second column block (see GemmDesc)
@@ -361,6 +363,27 @@ __device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int 
     }
 }
 
+// Tile order: bands of g.band tile columns, each band row-major.  The XCD
+// groups take consecutive ranges of this order, so a group's tiles cover a
+// roughly square block of C and share both operands' rows in its L2 (the
+// host picks the band width that minimises the operand bytes per group).
+__device__ __forceinline__ void tile_of(const GemmArgs &g, int lin, int &tm, int &tn)
+{
+    const int tiles_m = g.ntiles / g.tiles_n;
+    const int full = g.tiles_n / g.band;
+    const int per_band = tiles_m * g.band;
+    const int b = lin / per_band;
+    if (b < full) {
+        const int r = lin - b * per_band;
+        tm = r / g.band;
+        tn = b * g.band + r % g.band;
+    } else {   // the narrower last band
+        const int r = lin - full * per_band, wl = g.tiles_n - full * g.band;
+        tm = r / wl;
+        tn = full * g.band + r % wl;
+    }
+}
+
 // NWM x NWN waves; wave (wm, wn) owns the (BM/NWM) x (BN/NWN) block of the tile.
 // CB: the instantiation used when C is accumulated into (beta = 1, no split).
 // GT: fused cell update (GemmDesc::cell_h): tile columns are cell-major gates
@@ -387,7 +410,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
         run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
         return;
     }
-    const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
+    int tm, tn;
+    tile_of(g, tile, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     // second column block: its own B operand segments, k range and output
     constexpr bool DUAL_OK = !AK && !BKM;
@@ -626,6 +650,34 @@ __global__ __launch_bounds__(256) void splitk_reduce4(const float *__restrict__ 
     }
 }
 
+// Band width (tile columns) for the tile order: a group of `per_xcd` tiles
+// arranged (per_xcd / w) x w reads about per_xcd/w * BM rows of A and w * BN
+// rows of B; the power of two nearest sqrt(per_xcd * BM / BN) minimises the
+// sum.  Bands are used only where they cut that sum by a third or more
+// (BigLSTM's input projection: 5x; the headline layer's: 1.33x, where the
+// changed cache contents slowed the next kernels by more than they saved).
+// LSTM355_GEMM_BAND overrides (tests and tuning).
+int band_width(int tiles_m, int tiles_n, int per_xcd, int BM, int BN)
+{
+    auto rows_read = [&](int w) {
+        const int w_eff = w < tiles_n ? w : tiles_n;
+        const double rows_of_a = std::min((double)tiles_m, std::ceil((double)per_xcd / w_eff)) * BM;
+        return rows_of_a + (double)std::min(per_xcd, w_eff) * BN;
+    };
+    const char *env = std::getenv("LSTM355_GEMM_BAND");
+    int w = 0;
+    if (env) {
+        w = std::atoi(env);
+    } else {
+        const double best = std::sqrt((double)per_xcd * BM / BN);
+        w = 1;
+        while (w * 2 <= tiles_n && (double)(w * 2) <= best * 1.4142) w *= 2;
+        if (rows_read(tiles_n) < 1.5 * rows_read(w)) w = tiles_n;
+    }
+    if (w < 1 || w > tiles_n) w = tiles_n;
+    return w;
+}
+
 template <typename TO>
 hipError_t launch_splitk_reduce(const GemmDesc &d, int splits, hipStream_t s)
 {
@@ -657,6 +709,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.tiles_n = (d.N + BN - 1) / BN;
     g.ntiles = tiles_m * g.tiles_n;
     g.per_xcd = (g.ntiles + 7) / 8;
+    g.band = band_width(tiles_m, g.tiles_n, g.per_xcd, BM, BN);
     g.kchunk = ((d.K + splits - 1) / splits + KD - 1) / KD * KD;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
@@ -694,6 +747,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     g.tiles_n = (d.N + BN - 1) / BN;
     g.ntiles = tiles_m * g.tiles_n;
     g.per_xcd = (g.ntiles + 7) / 8;
+    g.band = g.tiles_n;
     g.kchunk = ((d.K + splits - 1) / splits + KS - 1) / KS * KS;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
