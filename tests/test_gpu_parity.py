@@ -115,12 +115,16 @@ LAYER_CASES = [
     (6, 33, 48, 136, 40, "bf16", True),    # LSTMP reverse, ragged
     (3, 130, 64, 96, 0, "bf16", False),    # more batch tiles than one workgroup row
     (1, 3, 16, 16, 0, "f32", False),       # a single step
+    (1, 1, 8, 8, 0, "f32", False),         # the smallest accepted layer: one step, one row, 8 wide
+    (3, 1, 8, 8, 0, "bf16", True),         # one batch row, reverse
     # XCD-local kernels (bf16, H in {256, 512, 1024}): ragged rows per XCD
     (6, 40, 64, 256, 0, "bf16", False),    # 5 rows per XCD
     (4, 130, 32, 512, 0, "bf16", True),    # 17 rows per XCD: two row blocks, reverse
     (3, 500, 40, 256, 0, "bf16", False),   # 63 rows per XCD: four row blocks
     (5, 16, 48, 1024, 0, "bf16", False),   # 2 rows per XCD, full-width cells
     (1, 9, 16, 256, 0, "bf16", True),      # a single step
+    (3, 3, 32, 256, 0, "bf16", False),     # fewer rows than XCDs: five XCDs own no row
+    (2, 1, 8, 1024, 0, "bf16", True),      # one row in all, full-width cells
     # [dW | dR] as one product (bf16, B a multiple of 32, I and I + H multiples of 128)
     (4, 32, 128, 256, 0, "bf16", False),   # with h0: the first step's segment comes from h0
     (3, 64, 128, 256, 0, "bf16", True),    # reverse: h0 pairs with the last time index
@@ -188,6 +192,36 @@ def test_stepwise_recurrence_parity(T, B, I, H, Hp, dtype, reverse, states, monk
     ref = oracle_layer(c, Hp, reverse)
     check_layer(gpu, ref, dtype, label)
     assert gpu["tiling"][3] == STEPWISE_VARIANT, gpu["tiling"]
+
+
+@pytest.mark.parametrize("dtype,H", [("f32", 40), ("bf16", 256), ("bf16", 1024)])
+def test_zero_weights_closed_form(dtype, H):
+    """W = R = 0 on the GPU against the closed form (no oracle): with
+    a = sigmoid(b_f), s = sigmoid(b_i) tanh(b_g), c_t = a c_{t-1} + s and
+    h_t = sigmoid(b_o) tanh(c_t), independent of x and h0; dx and dh0 are
+    exactly zero (every product has a zero operand)."""
+    T, B, I = 7, 24, 32
+    announce(f"zero weights closed form {dtype} H{H}")
+    c = layer_case(T, B, I, H, 0, dtype, False, seed=H + T)
+    zero = np.zeros((4 * H, I)), np.zeros((4 * H, H))
+    c["W"], c["R"] = synth.Tensor(zero[0], dtype), synth.Tensor(zero[1], dtype)
+    gpu = run_layer_gpu(c, T, B, I, H, 0, dtype, False)
+    b = c["b"].astype(np.float64)
+    sig = lambda u: 1.0 / (1.0 + np.exp(-u))
+    a, s_, so = sig(b[H:2 * H]), sig(b[:H]) * np.tanh(b[2 * H:3 * H]), sig(b[3 * H:])
+    cprev = c["c0"].astype(np.float64)
+    ys = []
+    for _ in range(T):
+        cprev = a * cprev + s_
+        ys.append(so * np.tanh(cprev))
+    y = np.stack(ys)
+    tol = TOL[dtype]["out"]
+    assert normwise(gpu["y"], y) <= tol, normwise(gpu["y"], y)
+    assert normwise(gpu["cT"], cprev) <= tol
+    assert np.all(gpu["dx"] == 0.0) and np.all(gpu["dh0"] == 0.0)
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        xcd = dtype == "bf16"
+        assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
 def test_layer_without_initial_state_or_final_grads():
