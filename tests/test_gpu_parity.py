@@ -319,3 +319,32 @@ def test_deterministic():
         for ga, gb in zip(la, lb):
             for k in ga:
                 assert np.array_equal(ga[k], gb[k]), k
+
+
+@pytest.mark.parametrize("dtype,n,off", [("bf16", 5040, 0), ("bf16", 1003, 0), ("bf16", 4096, 1), ("f32", 4099, 0),
+                                         ("f32", 4096, 0)])
+def test_add_bitwise(dtype, n, off):
+    """lstm_add (residual adds, summed input gradients): the fp32 sum of each
+    pair rounded once to the storage type, bit for bit, on the 16-byte path
+    (n a multiple of the vector width, aligned) and the element path (a
+    ragged n, or a view one element off alignment); in place as well."""
+    from paper_1907_13257_amd.lstm355 import lstm_add
+    announce(f"add {dtype} n{n} off{off}")
+    rng = np.random.default_rng(n + off)
+    a = synth.Tensor(rng.standard_normal(n + off), dtype)
+    b = synth.Tensor(rng.standard_normal(n + off), dtype)
+    da, db = to_dev(a)[off:], to_dev(b)[off:]
+    out = torch.empty_like(da)
+    lstm_add(dtype, n, da, db, out)
+    s32 = (a.f64[off:].astype(np.float32) + b.f64[off:].astype(np.float32))
+    if dtype == "bf16":
+        want = synth.f32_to_bf16_bits(s32)
+        got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    else:
+        want = s32.view(np.uint32)
+        got = out.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got, want)
+    lstm_add(dtype, n, da, db, da)   # out aliasing a
+    got2 = (da.view(torch.int16).cpu().numpy().view(np.uint16) if dtype == "bf16"
+            else da.cpu().numpy().view(np.uint32))
+    assert np.array_equal(got2, want)
