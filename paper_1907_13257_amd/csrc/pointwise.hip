@@ -25,6 +25,33 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ sr
     run_side_job(side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
 }
 
+// 16-bit elements, rows and cols multiples of 64, 16-byte aligned: 16-byte
+// loads along the source rows and 16-byte stores along the destination rows.
+__global__ __launch_bounds__(256) void transpose_u16_vec_kernel(const uint16_t *__restrict__ src, int rows, int cols,
+                                                                uint16_t *__restrict__ dst, SideJob side)
+{
+    __shared__ uint16_t tile[64][72];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int t = threadIdx.x, q = t & 7;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int i = p * 32 + (t >> 3);
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(src + (long)(r0 + i) * cols + c0 + q * 8);
+        *reinterpret_cast<u32x4 *>(&tile[i][q * 8]) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int i = p * 32 + (t >> 3);   // destination row c0 + i, source rows r0 + q*8 .. +8
+        unsigned w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            w[e] = (unsigned)tile[q * 8 + 2 * e][i] | ((unsigned)tile[q * 8 + 2 * e + 1][i] << 16);
+        *reinterpret_cast<u32x4 *>(dst + (long)(c0 + i) * rows + r0 + q * 8) = u32x4{w[0], w[1], w[2], w[3]};
+    }
+    run_side_job(side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+}
+
 __global__ void fill_kernel(uint32_t *p, size_t n, uint32_t v)
 {
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
@@ -225,6 +252,12 @@ hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hi
     ProfScope ps(K_SMALL, s, 0.0, 2.0 * rows * (double)cols * dsize(t));
     dim3 grid((cols + 63) / 64, (rows + 63) / 64);
     const SideJob sj = side ? *side : SideJob{};
+    if (t == DType::BF16 && rows % 64 == 0 && cols % 64 == 0 &&
+        ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0) {
+        hipLaunchKernelGGL(transpose_u16_vec_kernel, grid, dim3(256), 0, s, static_cast<const uint16_t *>(src), rows,
+                           cols, static_cast<uint16_t *>(dst), sj);
+        return hipGetLastError();
+    }
     if (t == DType::BF16)
         hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t *>(src), rows,
                            cols, static_cast<bf16_t *>(dst), sj);
