@@ -367,9 +367,13 @@ struct XBwdArgs {
 };
 
 // Per-cell inputs of one BPTT step (saved forward state and upstream gradient).
+// dy stays in its storage bits until it is used: converting it where it is
+// loaded would make the wave wait for that load, and with it for the dz
+// stores issued before it, ahead of the exchange copy.
 template <int MBX>
 struct BwdIn {
-    float dy[MBX], g[MBX][4], c[MBX], cp[MBX];
+    bf16_t dy[MBX];
+    float g[MBX][4], c[MBX], cp[MBX];
 };
 
 // Wave w multiplies the k range [w*H/2, (w+1)*H/2) of dh_{t-1} = R^T dz_t
@@ -418,7 +422,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             const int b = row0 + mb * 16 + cr;
             const bool v = has_cell && b < rowend;
             const long rt = (long)t * B + (v ? b : 0);
-            in.dy[mb] = v ? to_f32(a.dy[rt * a.ldy + cj]) : 0.0f;
+            in.dy[mb] = v ? a.dy[rt * a.ldy + cj] : (bf16_t)0;
 #pragma unroll
             for (int g = 0; g < 4; ++g) in.g[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
             in.c[mb] = v ? a.cs[rt * H + cj] : 0.0f;
@@ -443,31 +447,36 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 
     for (int s = a.T - 1; s >= 0; --s) {
         const int t = a.reverse ? a.T - 1 - s : s;
-        // gate gradients of the owned cells
+        // gate gradients of the owned cells.  Every lane computes them (lanes
+        // without a cell or row loaded zeros) and only the stores depend on
+        // the lane: each prefetched input is then consumed on every path, and
+        // the next prefetch does not wait for the previous one (nor for the
+        // dz stores issued after it) before the exchange copy.
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             const int b = row0 + mb * 16 + cr;
-            if (has_cell && b < rowend) {
-                const float ig = in.g[mb][0], fg = in.g[mb][1], gg = in.g[mb][2], og = in.g[mb][3];
-                const float dm = in.dy[mb] + dhn[mb];
-                const float tc = tanh_f(in.c[mb]);
-                const float d_o = dm * tc;
-                const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
-                const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * in.cp[mb];
-                const float zi = d_i * ig * (1.0f - ig), zf = d_f * fg * (1.0f - fg);
-                const float zg = d_g * (1.0f - gg * gg), zo = d_o * og * (1.0f - og);
+            const bool v = has_cell && b < rowend;
+            const float ig = in.g[mb][0], fg = in.g[mb][1], gg = in.g[mb][2], og = in.g[mb][3];
+            const float dm = to_f32(in.dy[mb]) + dhn[mb];
+            const float tc = tanh_f(in.c[mb]);
+            const float d_o = dm * tc;
+            const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
+            const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * in.cp[mb];
+            const float zi = d_i * ig * (1.0f - ig), zf = d_f * fg * (1.0f - fg);
+            const float zg = d_g * (1.0f - gg * gg), zo = d_o * og * (1.0f - og);
+            if (v) {
                 bf16_t *dzp = a.dz + ((long)t * B + b) * G4 + cj;
                 dzp[0] = ready_value(f32_to_bf16(zi));
                 dzp[H] = ready_value(f32_to_bf16(zf));
                 dzp[2 * H] = ready_value(f32_to_bf16(zg));
                 dzp[3 * H] = ready_value(f32_to_bf16(zo));
-                dbacc[0] += zi;
-                dbacc[1] += zf;
-                dbacc[2] += zg;
-                dbacc[3] += zo;
-                dcn[mb] = d_c * fg;
-                if (s == 0 && a.dc0) a.dc0[(long)b * H + cj] = dcn[mb];
             }
+            dbacc[0] += v ? zi : 0.0f;
+            dbacc[1] += v ? zf : 0.0f;
+            dbacc[2] += v ? zg : 0.0f;
+            dbacc[3] += v ? zo : 0.0f;
+            dcn[mb] = d_c * fg;
+            if (v && s == 0 && a.dc0) a.dc0[(long)b * H + cj] = dcn[mb];
         }
         if (s == 0 && !a.dh0) break;
         // the next step's inputs travel while this step's dz is exchanged
