@@ -323,19 +323,26 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                 *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
             __syncthreads();
             if (s_bad) return;   // the same decision in every wave
+            // Every lane applies the cell equations (a lane without a cell reads
+            // row 0 of the partial sums; lanes without a cell or row produce
+            // values nobody stores) and only the stores depend on the lane:
+            // the input projection loaded for this step is then consumed on
+            // every path, and the next step's loads do not wait for these
+            // loads, nor for the stores issued after them.
             const int b = rb0 + cr;
+            const int crr = has_cell ? cr : 0;
+            float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
+#pragma unroll
+                for (int g = 0; g < 4; ++g) z[g] += p[g];
+            }
+            const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+            const float c = fg * creg[mb] + ig * gg;
+            const float m = og * tanh_f(c);
+            creg[mb] = c;
             if (has_cell && b < rowend) {
-                float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][cr][4 * cu]);
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) z[g] += p[g];
-                }
-                const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-                const float c = fg * creg[mb] + ig * gg;
-                const float m = og * tanh_f(c);
-                creg[mb] = c;
                 const bf16_t hv = ready_value(f32_to_bf16(m));
                 a.y[((long)t * B + b) * a.ldy + cj] = hv;
                 if (last && a.hT) a.hT[(long)b * H + cj] = hv;
