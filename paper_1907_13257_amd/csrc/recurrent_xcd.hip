@@ -328,32 +328,36 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
             // values nobody stores) and only the stores depend on the lane:
             // the input projection loaded for this step is then consumed on
             // every path, and the next step's loads do not wait for these
-            // loads, nor for the stores issued after them.
+            // loads, nor for the stores issued after them.  With four row
+            // blocks the registers run short and the lanes without a row skip it.
+            constexpr bool ALL_LANES = MBX <= 2;
             const int b = rb0 + cr;
             const int crr = has_cell ? cr : 0;
-            float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
+            if (ALL_LANES || (has_cell && b < rowend)) {
+                float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
+                for (int q = 0; q < 8; ++q) {
+                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
 #pragma unroll
-                for (int g = 0; g < 4; ++g) z[g] += p[g];
-            }
-            const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-            const float c = fg * creg[mb] + ig * gg;
-            const float m = og * tanh_f(c);
-            creg[mb] = c;
-            if (has_cell && b < rowend) {
-                const bf16_t hv = ready_value(f32_to_bf16(m));
-                a.y[((long)t * B + b) * a.ldy + cj] = hv;
-                if (last && a.hT) a.hT[(long)b * H + cj] = hv;
-                // saved activations for the backward pass (not on the critical path)
-                float *gp = a.gates + ((long)t * B + b) * G4 + cj;
-                gp[0] = ig;
-                gp[H] = fg;
-                gp[2 * H] = gg;
-                gp[3 * H] = og;
-                a.cs[((long)t * B + b) * H + cj] = c;
-                if (last && a.cT) a.cT[(long)b * H + cj] = c;
+                    for (int g = 0; g < 4; ++g) z[g] += p[g];
+                }
+                const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+                const float c = fg * creg[mb] + ig * gg;
+                const float m = og * tanh_f(c);
+                creg[mb] = c;
+                if (has_cell && b < rowend) {
+                    const bf16_t hv = ready_value(f32_to_bf16(m));
+                    a.y[((long)t * B + b) * a.ldy + cj] = hv;
+                    if (last && a.hT) a.hT[(long)b * H + cj] = hv;
+                    // saved activations for the backward pass (not on the critical path)
+                    float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+                    gp[0] = ig;
+                    gp[H] = fg;
+                    gp[2 * H] = gg;
+                    gp[3 * H] = og;
+                    a.cs[((long)t * B + b) * H + cj] = c;
+                    if (last && a.cT) a.cT[(long)b * H + cj] = c;
+                }
             }
             __syncthreads();   // red is rewritten by the next row block or step
         }
@@ -458,11 +462,14 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
         // without a cell or row loaded zeros) and only the stores depend on
         // the lane: each prefetched input is then consumed on every path, and
         // the next prefetch does not wait for the previous one (nor for the
-        // dz stores issued after it) before the exchange copy.
+        // dz stores issued after it) before the exchange copy.  With four row
+        // blocks the registers run short and the lanes without a row skip it.
+        constexpr bool ALL_LANES = MBX <= 2;
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             const int b = row0 + mb * 16 + cr;
             const bool v = has_cell && b < rowend;
+            if (!ALL_LANES && !v) continue;
             const float ig = in.g[mb][0], fg = in.g[mb][1], gg = in.g[mb][2], og = in.g[mb][3];
             const float dm = to_f32(in.dy[mb]) + dhn[mb];
             const float tc = tanh_f(in.c[mb]);
