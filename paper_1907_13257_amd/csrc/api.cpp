@@ -316,7 +316,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         // [dW | dR] = dZ^T [X | H_prev] as one product when the shapes allow
         // (H_prev: y of the previous visited step, h0 for the first one)
         bool fused = false;
-        if (h->dt == DType::BF16 && B % 32 == 0 && T > 1) {
+        if (h->dt == DType::BF16 && (B % 32 == 0 || !h0) && T > 1) {
             GemmDesc g{};
             g.in = h->dt; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
             g.M = (int)G4; g.N = I + Hr; g.K = (int)TB;

@@ -433,7 +433,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
     DmaOperand<BM, AK, KD, NW> da;
     DmaOperand<BN, BKM, KD, NW> db;    // B, or B2 for the second block
     DmaOperand<BN, BKM, KD, NW> dh;    // B3 (second block only)
-    da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)g.K * g.lda * 2);
+    // (second block without an h0 segment: rows of A past its k range read
+    // zero, so a last stage that reaches past it adds nothing)
+    da.init(g.A, g.lda, m0, AK ? (long)g.M * g.lda * 2 : (long)(second && !g.B3 ? g.yhi : g.K) * g.lda * 2);
     if (!second) {
         db.init(g.B, g.ldb, n0, BKM ? (long)g.N * g.ldb * 2 : (long)g.K * g.ldb * 2);
         if (GT) db.ilv = g.cell_h;
@@ -983,7 +985,8 @@ bool tile_fits(const GemmDesc &d, int t)
     if (d.K % kd && (d.a_kmajor || d.b_kmajor)) return false;
     if ((!d.a_kmajor && kTileBM[t] < 128) || (!d.b_kmajor && kTileBN[t] < 128)) return false;
     if (d.N1 > 0 && (d.N1 % kTileBN[t] || d.N % kTileBN[t] || d.M % kTileBM[t])) return false;
-    if (d.N1 > 0 && (d.ylo % kd || d.yhi % kd || d.hlo % kd || d.hlen % kd)) return false;   // stages stay in one segment
+    if (d.N1 > 0 && d.B3 && (d.ylo % kd || d.yhi % kd || d.hlo % kd || d.hlen % kd))
+        return false;   // stages stay in one segment
     return dl_ok(d, kTileBM[t], kTileBN[t], 1);
 }
 
@@ -1054,9 +1057,11 @@ hipError_t dispatch_layout(const GemmDesc &d, hipStream_t s)
 bool gemm_dual_ok(const GemmDesc &d)
 {
     if (d.in != DType::BF16 || d.a_kmajor || d.b_kmajor || !d.out_f32) return false;
-    if (d.N1 <= 0 || d.N1 >= d.N || d.N1 % 128 || d.N % 128 || d.M % 128 || d.K % 32) return false;
-    if (d.ylo % 32 || d.yhi % 32 || d.hlo % 32 || d.hlen % 32 || d.ylo < 0 || d.yhi > d.K || d.ylo >= d.yhi)
-        return false;
+    if (d.N1 <= 0 || d.N1 >= d.N || d.N1 % 128 || d.N % 128 || d.M % 128) return false;
+    if (d.ylo < 0 || d.yhi > d.K || d.ylo >= d.yhi) return false;
+    // with an h0 segment, stages of 32 k must not straddle a segment boundary;
+    // without one, the second block runs over [ylo, yhi) alone
+    if (d.B3 && (d.K % 32 || d.ylo % 32 || d.yhi % 32 || d.hlo % 32 || d.hlen % 32)) return false;
     if (d.B3 && (d.hlo < 0 || d.hlo + d.hlen > d.K)) return false;
     return dl_ok(d, 128, 128, 1);
 }

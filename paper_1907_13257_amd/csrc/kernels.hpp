@@ -77,8 +77,9 @@ struct GemmDesc {
     //   C2[m][n-N1] (+)= sum over k of A(m,k) * S(n-N1, k), where row k of the
     //   operand S is B3 row (k - hlo) for k in [hlo, hlo+hlen) (skipped when
     //   B3 is NULL) and B2 row (k + yoff) for k in [ylo, yhi).
-    // Stages of 32 k never straddle those ranges (hlo, hlen, ylo, yhi are
-    // multiples of 32).
+    // With B3, stages of 32 k never straddle those ranges (hlo, hlen, ylo,
+    // yhi are multiples of 32).  Without B3 the second block runs over
+    // [ylo, yhi) alone, from any ylo (rows of A past yhi read as zero).
     int N1 = 0;                // 0: no second block
     const void *B2 = nullptr; long ldb2 = 0; long b2_bytes = 0;
     const void *B3 = nullptr; long ldb3 = 0; long b3_bytes = 0;

@@ -233,10 +233,13 @@ def test_layer_without_initial_state_or_final_grads():
     check_layer(gpu, ref, "f32", "zero states")
 
 
-def test_fused_weight_gradients_without_h0_and_accumulating():
+@pytest.mark.parametrize("T,B", [(4, 32), (5, 16), (3, 24), (4, 8)])
+def test_fused_weight_gradients_without_h0_and_accumulating(T, B):
     """[dW | dR] as one product with no initial state (the first step's
-    segment is skipped), then accumulated into existing gradients."""
-    T, B, I, H = 4, 32, 128, 256
+    segment is skipped; without it any batch size runs fused, the k range of
+    the second block then starting and ending off the 32-deep stages), then
+    accumulated into existing gradients."""
+    I, H = 128, 256
     for reverse in (False, True):
         announce(f"fused dW|dR zero state rev{int(reverse)}")
         c = layer_case(T, B, I, H, 0, "bf16", reverse, seed=11 + reverse, states=False, final_grads=False)
