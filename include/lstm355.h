@@ -90,6 +90,30 @@ lstm_status_t lstm_forward(lstm_handle_t h,
                            void *y, void *hT, float *cT,
                            void *reserve, void *workspace, void *stream);
 
+/* Forward pass of a stack of L unidirectional LSTM layers run as one layer
+ * wavefront: layer l+1 starts a time step as soon as layer l has produced
+ * that step, so the layers advance together a few steps apart instead of one
+ * after another.  This is the pipelining of layers over the sequence that
+ * the paper uses for model parallelism of GNMT and BigLSTM (Section 2,
+ * "Background"; Section 4, "Model Parallel Splitting"), here spread over the
+ * XCDs of one GPU.  The result equals L calls of lstm_forward with
+ * x_{l+1} = y_l, zero initial states and no final states.
+ *   h[l]: handles of the layers (bf16, Hp = 0, not reversed, equal T, B, H;
+ *     layer l >= 1 has I = H and dense x and y).
+ *   x: the stack's input, as for lstm_forward on h[0].
+ *   W[l], R[l], b[l]: parameters of layer l.
+ *   y[l]: output of layer l [T][B][H] (the input of layer l+1).
+ *   reserve[l]: reserve of layer l (lstm_reserve_size(h[l]) bytes), for
+ *     lstm_backward on h[l] exactly as after lstm_forward.
+ *   workspace: at least the largest lstm_workspace_size of the handles.
+ * Runs when L is 2..4, H = 1024 and B <= 16 on an MI355X whose XCD-local
+ * path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the caller
+ * runs the layers one by one with lstm_forward (which rewrites anything this
+ * call may have written). */
+lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *h, const void *x,
+                                 const void *const *W, const void *const *R, const float *const *b,
+                                 void *const *y, void *const *reserve, void *workspace, void *stream);
+
 /* Back-propagation through time for the loss
  *   L = sum_t <dy_t, y_t> + <dhT, h_final> + <dcT, c_final>,
  * summed over the batch.  Needs the forward's x, h0, c0 (the same values),

@@ -243,6 +243,70 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
     }
 }
 
+extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, const void *x, const void *const *W,
+                                            const void *const *R, const float *const *b, void *const *y,
+                                            void *const *reserve, void *workspace, void *stream)
+{
+    try {
+        if (L < 1 || !hs || !x || !W || !R || !b || !y || !reserve || !workspace)
+            return invalid("required pointer is NULL or L < 1");
+        for (int l = 0; l < L; ++l) {
+            if (!hs[l] || !W[l] || !R[l] || !b[l] || !y[l] || !reserve[l]) return invalid("required pointer is NULL");
+            for (const void *p : {W[l], R[l], (const void *)y[l], (const void *)reserve[l]})
+                if (!aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+            if (!aligned4(b[l])) return invalid("fp32 tensors must be 4-byte aligned");
+        }
+        if (!aligned16(x) || !aligned16(workspace)) return invalid("device tensors must be 16-byte aligned");
+        auto unsupported = [](const char *why) {
+            std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: %s", why);
+            return LSTM_ERR_UNSUPPORTED;
+        };
+        if (L < 2 || L > 4) return unsupported("needs 2 to 4 layers");
+        const lstm_desc_t &d0 = hs[0]->d;
+        for (int l = 0; l < L; ++l) {
+            const lstm_desc_t &d = hs[l]->d;
+            if (hs[l]->dt != DType::BF16 || d.Hp != 0 || d.reverse != 0) return unsupported("bf16 LSTM layers only");
+            if (d.T != d0.T || d.B != d0.B || d.H != d0.H) return unsupported("layers differ in T, B or H");
+            if (l > 0 && (d.I != d.H || hs[l]->ldx != d.H)) return unsupported("a layer's input is not the layer below");
+        }
+        for (int l = 0; l < L; ++l) {   // the checks that query the device
+            const lstm_desc_t &d = hs[l]->d;
+            RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, hs[l]->ldy};
+            lstm_status_t st = ensure_plan(hs[l]);
+            if (st != LSTM_OK) return st;
+            if (!wave_path_ok(sh, hs[l]->num_cus)) return unsupported("shape or device");
+        }
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        lstm_handle *h0 = hs[0];
+        char *wv = static_cast<char *>(workspace);
+        WaveBufs wb[4];
+        for (int l = 0; l < L; ++l) {
+            char *rv = static_cast<char *>(reserve[l]);
+            wb[l].R = R[l];
+            wb[l].W = W[l];
+            wb[l].bias = b[l];
+            wb[l].gates = reinterpret_cast<float *>(rv + hs[l]->r_gates);
+            wb[l].cs = reinterpret_cast<float *>(rv + hs[l]->r_cs);
+            wb[l].y = y[l];
+        }
+        // layer 0's input projection as in lstm_forward; the others are computed in the wavefront
+        GemmDesc g{};
+        g.in = DType::BF16; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
+        g.M = (int)h0->TB; g.N = (int)h0->G4; g.K = d0.I;
+        g.A = x; g.lda = h0->ldx;
+        g.B = W[0]; g.ldb = d0.I;
+        g.C = wb[0].gates; g.ldc = h0->G4;
+        g.bias = b[0]; g.beta = 0;
+        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+        RecShape sh{d0.T, d0.B, d0.I, d0.H, 0, 0, h0->ldy};
+        TRY_HIP("layer wavefront", launch_forward_wave(sh, L, wb, reinterpret_cast<unsigned *>(wv + h0->w_sync),
+                                                       watchdog_ticks(), s));
+        return LSTM_OK;
+    } catch (...) {
+        return invalid("exception");
+    }
+}
+
 extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const void *dhT, const float *dcT,
                                        const void *x, const void *h0, const float *c0, const void *W, const void *R,
                                        const void *P, const void *y, const void *reserve, void *dx, void *dh0,

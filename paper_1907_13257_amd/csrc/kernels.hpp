@@ -213,6 +213,20 @@ unsigned long long watchdog_ticks();
 // earlier launch on the stream (xcd_prep_forward / xcd_prep_backward as a
 // side job) already did.
 constexpr uint16_t XCD_NOT_READY = 0xffffu;
+// Layer wavefront forward of a stack of L (2..4) unidirectional bf16 layers
+// (H = 1024, at most 16 batch rows, zero initial states, y dense): layer 0's
+// input projection must already be in ly[0].gates (with bias); layers >= 1
+// take their input from the layer below.  Fills the exchanged rows and the
+// flags itself.
+struct WaveBufs {
+    const void *R, *W;
+    const float *bias;
+    float *gates, *cs;
+    void *y;
+};
+bool wave_path_ok(const RecShape &sh, int num_cus);
+hipError_t launch_forward_wave(const RecShape &sh, int L, const WaveBufs *ly, unsigned *sync,
+                               unsigned long long timeout, hipStream_t s);
 SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
 SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);
 hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s,

@@ -365,6 +365,207 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Layer wavefront: the forward pass of a stack of L (2..4) unidirectional
+// layers in one launch, for batches of at most 16 rows (all rows in one
+// XCD).  XCD 2l runs layer l's recurrence with the rows of R_l resident, as
+// lstm_fwd_xcd does with all rows in one XCD; XCD 2l+1 (l >= 1) keeps the
+// rows of W_l resident and computes each step's input projection y_{l-1,t}
+// W_l^T + b_l as soon as layer l-1 has produced y_{l-1,t}.  The layers thus
+// advance together, a few steps apart, instead of one after another (the
+// pipelining of layers over time steps that model parallelism exploits).
+// Rows that cross XCDs (y into the next layer's projection, the projection
+// into the recurrence) are stored with device-coherent (sc1) stores and read
+// with sc1 loads under the NOT_READY protocol: y is filled with the bf16
+// pattern, the projections of layers >= 1 with the fp32 pattern 0xffffffff,
+// before the launch.  Layer 0's projection comes from the GEMM as usual.
+struct WaveLayer {
+    const bf16_t *R, *W;
+    const float *bias;
+    float *gates, *cs;   // gates: the input projection in, the activations out
+    bf16_t *y;           // [T][B][H]
+};
+
+struct XWaveArgs {
+    int T, B, H, L;
+    WaveLayer ly[4];
+    unsigned *flags;
+    unsigned long long timeout;
+};
+
+constexpr unsigned NOT_READY_F32 = 0xffffffffu;
+
+__device__ __forceinline__ unsigned ready_f32(float v)
+{
+    const unsigned u = __float_as_uint(v);
+    return u == NOT_READY_F32 ? 0x7fc00000u : u;
+}
+
+template <int HN>
+__global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
+{
+    constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
+    constexpr int NB = NT / 16;
+    constexpr int KW = 4 * HN;        // k per wave (H / 8)
+    constexpr int KCW = KW / 32;
+    constexpr int RB = KW * 2;
+    constexpr int NCELL = 16 * HN;
+    constexpr int RP = NT + 36;
+    __shared__ __attribute__((aligned(16))) float red[8][16][RP];
+    __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
+    __shared__ int s_xcd;
+    __shared__ int s_bad;
+
+    if (!claim_role(a.flags, &s_xcd)) return;
+    const int xcd = s_xcd, layer = xcd >> 1;
+    const bool wrole = (xcd & 1) != 0;
+    if (layer >= a.L || (wrole && layer == 0)) return;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, slot = blockIdx.x >> 3;
+    const int H = a.H, B = a.B;
+    const long G4 = 4L * H;
+    const int j0 = slot * HN;
+    const unsigned tile = lds_addr(&stage[w][0]);
+    const WaveLayer ly = a.ly[layer];
+
+    // resident weights: the 4*HN rows of R_l (recurrence) or W_l (projection)
+    // feeding the owned cells, cell-major (row 4u + g), this wave's k range
+    const bf16_t *M = wrole ? ly.W : ly.R;
+    u32x4 rf[NB][KCW];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int n = i * 16 + (lane & 15);
+        const int g = n & 3, u = n >> 2;
+        const bf16_t *rrow = M + (long)(g * H + j0 + u) * H + w * KW;
+#pragma unroll
+        for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + c * 32 + (lane >> 4) * 8);
+    }
+    const bool has_cell = tid < NCELL;
+    const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
+    const int crr = has_cell ? cr : 0;
+    const bool vrow = has_cell && cr < B;
+    // bounded descriptors: lanes without a row read rows past the last step
+    // at the end (those loads return zero), and no store leaves its tensor
+    const __amdgpu_buffer_rsrc_t rg =
+        __builtin_amdgcn_make_buffer_rsrc(ly.gates, (short)0, (int)((long)a.T * B * G4 * 4), 0x00020000);
+    if (tid == 0) s_bad = 0;   // ordered by the first barrier below
+
+    if (wrole) {
+        // input projection of layer l from the rows of y_{l-1}
+        const u32x4 rs_x = buffer_desc(a.ly[layer - 1].y, (long)a.T * B * H * 2);
+        float bz[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) bz[g] = has_cell ? ly.bias[g * H + cj] : 0.0f;
+        for (int s = 0; s < a.T; ++s) {
+            f32x4 acc[NB];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B, H, w * KW * 2, tile, stage[w], lane, B,
+                                                         rf, acc, a.flags, a.timeout, slot))
+                s_bad = 1;
+#pragma unroll
+            for (int i = 0; i < NB; ++i)
+                *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
+            __syncthreads();
+            if (s_bad) return;
+            if (vrow) {
+                float z[4] = {bz[0], bz[1], bz[2], bz[3]};
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][cr][4 * cu]);
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) z[g] += p[g];
+                }
+                const unsigned off = (unsigned)((((long)s * B + cr) * G4 + cj) * 4);
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    __builtin_amdgcn_raw_buffer_store_b32(ready_f32(z[g]), rg, off + (unsigned)(g * H * 4), 0, 16);
+            }
+            __syncthreads();   // red is rewritten by the next step
+        }
+        return;
+    }
+
+    // recurrence of layer l
+    const u32x4 rs_y = buffer_desc(ly.y, (long)a.T * B * H * 2);
+    const __amdgpu_buffer_rsrc_t ryw =
+        __builtin_amdgcn_make_buffer_rsrc(ly.y, (short)0, (int)((long)a.T * B * H * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
+    const bool poll_gx = layer > 0;
+    float creg = 0.0f;
+    for (int s = 0; s < a.T; ++s) {
+        // this step's input projection (layers > 0: may still be in flight)
+        const unsigned goff = (unsigned)((((long)s * B + crr) * G4 + cj) * 4);
+        unsigned gxu[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            gxu[g] = poll_gx ? __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16)
+                             : __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 0);
+        f32x4 acc[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (s > 0) {
+            if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_y, (long)(s - 1) * B, H, w * KW * 2, tile, stage[w], lane,
+                                                         B, rf, acc, a.flags, a.timeout, slot))
+                s_bad = 1;
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
+        __syncthreads();
+        if (s_bad) return;
+        if (poll_gx) {   // re-read the elements that still hold NOT_READY
+            const unsigned long long t0 = wall_clock64();
+            while (true) {
+                bool nr = false;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) nr = nr || (vrow && gxu[g] == NOT_READY_F32);
+                if (__builtin_amdgcn_ballot_w64(nr) == 0) break;
+                const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+                if (ab != 0 || wall_clock64() - t0 > a.timeout) {
+                    if (lane == 0 && ab == 0) {
+                        __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    s_bad = 1;
+                    break;
+                }
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    if (vrow && gxu[g] == NOT_READY_F32)
+                        gxu[g] = __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16);
+            }
+        }
+        {
+            float z[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) z[g] = __uint_as_float(gxu[g]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
+#pragma unroll
+                for (int g = 0; g < 4; ++g) z[g] += p[g];
+            }
+            const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+            const float c = fg * creg + ig * gg;
+            const float m = og * tanh_f(c);
+            creg = c;
+            if (vrow) {
+                const bf16_t hv = ready_value(f32_to_bf16(m));
+                __builtin_amdgcn_raw_buffer_store_b16(hv, ryw, (unsigned)((((long)s * B + cr) * H + cj) * 2), 0, 16);
+                // saved activations for the backward pass (not on the critical path)
+                float *gp = ly.gates + ((long)s * B + cr) * G4 + cj;
+                gp[0] = ig;
+                gp[H] = fg;
+                gp[2 * H] = gg;
+                gp[3 * H] = og;
+                ly.cs[((long)s * B + cr) * H + cj] = c;
+            }
+        }
+        __syncthreads();   // red is rewritten by the next step
+        if (s_bad) return;
+    }
+}
+
 struct XBwdArgs {
     int T, B, H, reverse, RX;
     long ldy;
@@ -601,6 +802,44 @@ bool xcd_path_ok(DType t, const RecShape &sh, int num_cus)
 }
 
 void xcd_path_disable() { g_xcd_disabled = 1; }
+
+bool wave_path_ok(const RecShape &sh, int num_cus)
+{
+    return !g_xcd_disabled && num_cus == NXCD * WG_PER_XCD && sh.H == 1024 && sh.Hp == 0 && sh.reverse == 0 &&
+           sh.B >= 1 && sh.B <= 16 && sh.ldy == sh.H && (long)sh.T * sh.B * 4L * sh.H * 4 <= 0x7fffffffL;
+}
+
+hipError_t launch_forward_wave(const RecShape &sh, int L, const WaveBufs *ly, unsigned *sync,
+                               unsigned long long timeout, hipStream_t s)
+{
+    if (L < 2 || L > 4) return hipErrorInvalidValue;
+    XWaveArgs a{};
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.L = L;
+    for (int l = 0; l < L; ++l) {
+        a.ly[l].R = static_cast<const bf16_t *>(ly[l].R);
+        a.ly[l].W = static_cast<const bf16_t *>(ly[l].W);
+        a.ly[l].bias = ly[l].bias;
+        a.ly[l].gates = ly[l].gates;
+        a.ly[l].cs = ly[l].cs;
+        a.ly[l].y = static_cast<bf16_t *>(ly[l].y);
+    }
+    a.flags = sync + XCD_FLAGS;
+    a.timeout = timeout;
+    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+    const long rows = (long)sh.T * sh.B;
+    for (int l = 0; l < L && e == hipSuccess; ++l) {
+        // every exchanged row waits for its producer: y of each layer, and
+        // the input projections that the projection XCDs write
+        e = fill_rows_u16(ly[l].y, rows, sh.H, sh.H, NOT_READY, s);
+        if (e == hipSuccess && l > 0) e = fill_u32(ly[l].gates, (size_t)rows * 4 * sh.H, NOT_READY_F32, s);
+    }
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (2 * L - 1),
+                 (double)L * (sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0) +
+                     (L - 1) * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
+    return launch256<lstm_fwd_wave<32>>(s, &a);
+}
 
 hipError_t xcd_tripped_read_and_clear(unsigned *tripped)
 {

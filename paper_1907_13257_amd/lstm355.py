@@ -57,6 +57,7 @@ def load_library():
         "lstm_workspace_size": ([H], sz),
         "lstm_forward": ([H] + [vp] * 13, i),
         "lstm_backward": ([H] + [vp] * 18 + [i, vp, vp], i),
+        "lstm_forward_stack": ([i] + [vp] * 9, i),
         "lstm_check": ([H, vp, vp], i),
         "lstm_destroy": ([H], i),
         "lstm_status_string": ([i], ctypes.c_char_p),
@@ -129,6 +130,20 @@ def lstm_forward(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, workspace, stream
     _check(load_library().lstm_forward(h, _ptr(x), _ptr(h0), _ptr(c0), _ptr(W), _ptr(R), _ptr(b), _ptr(P), _ptr(y),
                                        _ptr(hT), _ptr(cT), _ptr(reserve), _ptr(workspace), _stream(stream)),
            "lstm_forward")
+
+
+def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=None) -> bool:
+    """Layer-wavefront forward of a stack (lstm_forward_stack).  Returns False,
+    having computed nothing that counts, when the stack does not fit it
+    (LSTM_ERR_UNSUPPORTED); raises on any other error."""
+    n = len(handles)
+    arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
+    st = load_library().lstm_forward_stack(n, arr(handles), _ptr(x), arr(Ws), arr(Rs), arr(bs), arr(ys),
+                                           arr(reserves), _ptr(workspace), _stream(stream))
+    if st == LSTM_ERR_UNSUPPORTED:
+        return False
+    _check(st, "lstm_forward_stack")
+    return True
 
 
 def lstm_backward(h, dy, dhT, dcT, x, h0, c0, W, R, P, y, reserve, dx, dh0, dc0, dW, dR, db, dP, accumulate,
@@ -255,9 +270,11 @@ class Stack:
     params[l][d] = dict(W, R, b[, P]) device tensors; grads likewise with
     dW, dR, db[, dP] (fp32), allocated here."""
 
-    def __init__(self, T, B, layers: Sequence[StackLayer], dtype="bf16", device="cuda"):
+    def __init__(self, T, B, layers: Sequence[StackLayer], dtype="bf16", device="cuda", wavefront=True):
         import torch
         self.T, self.B, self.dtype, self.device = T, B, dtype, device
+        self.wavefront = wavefront
+        self.last_forward = None
         self.layers = list(layers)
         td = torch_dtype(dtype)
         self.dirs: List[List[Layer]] = []
@@ -300,6 +317,18 @@ class Stack:
         return grads
 
     def forward(self, x, params, stream=None):
+        # a stack of plain unidirectional layers runs as one layer wavefront
+        # when the library supports its shape (lstm_forward_stack)
+        self.last_forward = "layers"
+        if (self.wavefront and 2 <= len(self.layers) <= 4 and self.dtype == "bf16"
+                and all(not L.bidirectional and not L.residual and not L.Hp for L in self.layers)):
+            lays = [d[0] for d in self.dirs]
+            if lstm_forward_stack([l.handle for l in lays], x, [p[0]["W"] for p in params],
+                                  [p[0]["R"] for p in params], [p[0]["b"] for p in params], self.y,
+                                  [l.reserve for l in lays], self.workspace, stream):
+                self.inputs = [x] + self.y[:-1]
+                self.last_forward = "wavefront"
+                return self.y[-1]
         cur = x
         for li, L in enumerate(self.layers):
             self.inputs[li] = cur

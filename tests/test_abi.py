@@ -85,6 +85,36 @@ def test_forward_backward_validate_before_launch(lib):
     L.lstm_destroy(hp)
 
 
+def test_forward_stack_validates_before_launch(lib):
+    """lstm_forward_stack rejects bad arguments and stacks the layer
+    wavefront does not cover before anything touches the GPU."""
+    import ctypes
+    A = 1 << 20
+    hb = [L.lstm_create(4, 8, 1024, 1024, 0, "bf16") for _ in range(5)]
+    hf = [L.lstm_create(4, 8, 1024, 1024, 0, "f32") for _ in range(2)]
+    arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
+    ptrs = lambda n: arr([A] * n)
+
+    def call(hs, x=A, n=None):
+        n = len(hs) if n is None else n
+        return lib.lstm_forward_stack(n, arr(hs), x, ptrs(n), ptrs(n), ptrs(n), ptrs(n), ptrs(n), A, None)
+
+    assert call(hb[:2], x=None) == L.LSTM_ERR_INVALID_ARG                  # missing input
+    assert call(hb[:2], x=A + 2) == L.LSTM_ERR_INVALID_ARG                 # misaligned input
+    assert call(hb[:2], n=0) == L.LSTM_ERR_INVALID_ARG
+    assert call([hb[0], None]) == L.LSTM_ERR_INVALID_ARG                  # missing handle
+    assert call(hb[:1]) == L.LSTM_ERR_UNSUPPORTED                          # one layer
+    assert call(hb[:5]) == L.LSTM_ERR_UNSUPPORTED                          # five layers
+    assert call(hf) == L.LSTM_ERR_UNSUPPORTED                              # fp32
+    assert "wavefront" in L.lstm_last_error_detail()
+    hr = L.lstm_create(4, 8, 1024, 1024, 0, "bf16", reverse=True)
+    assert call([hb[0], hr]) == L.LSTM_ERR_UNSUPPORTED                     # a reversed layer
+    hw = L.lstm_create(4, 8, 512, 1024, 0, "bf16")
+    assert call([hb[0], hw]) == L.LSTM_ERR_UNSUPPORTED                     # layer 1 input is not layer 0's y
+    for h in hb + hf + [hr, hw]:
+        L.lstm_destroy(h)
+
+
 def test_add_validates(lib):
     assert lib.lstm_add(5, 4, 1 << 20, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG
     assert lib.lstm_add(1, 4, None, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG

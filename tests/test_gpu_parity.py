@@ -310,6 +310,47 @@ def test_small_lstmp_stack_parity():
     compare(gpu, ref, "bf16", label="small lstmp stack")
 
 
+WAVE_CASES = [
+    # (T, B, input width of layer 0, layers)
+    (6, 16, 1024, 2),
+    (5, 5, 512, 3),
+    (4, 13, 1024, 4),
+    (1, 16, 1024, 2),
+]
+
+
+@pytest.mark.parametrize("T,B,I0,nl", WAVE_CASES)
+def test_layer_wavefront_stack_parity(T, B, I0, nl):
+    """A stack of plain layers at B <= 16, H = 1024 runs its forward pass as
+    one layer wavefront (lstm_forward_stack); outputs and every gradient of
+    the following backward pass match the oracle."""
+    layers = [synth.LayerSpec(I0, 1024)] + [synth.LayerSpec(1024, 1024) for _ in range(nl - 1)]
+    wl = synth.Workload(f"wave_T{T}_B{B}_L{nl}", T=T, B=B, layers=layers, dtype="bf16", seed=11 + nl, w_scale=0.05)
+    announce(f"layer wavefront T={T} B={B} I0={I0} L={nl}")
+    prob = synth.draw(wl)
+    gpu, stack = run_stack_gpu(prob)
+    assert stack.last_forward == "wavefront"
+    ref = run_oracle(prob)
+    compare(gpu, ref, "bf16", label=wl.name)
+
+
+def test_layer_wavefront_matches_layer_by_layer():
+    """The wavefront and the layer-by-layer forward give the same outputs up
+    to the summation order of the input projection."""
+    from paper_1907_13257_amd import Stack
+    from _gpu_helpers import device_params, stack_layers
+    wl = synth.Workload("wave_vs_layers", T=8, B=16, layers=[synth.LayerSpec(1024, 1024) for _ in range(3)],
+                        dtype="bf16", seed=21, w_scale=0.05)
+    announce("layer wavefront vs layers")
+    prob = synth.draw(wl)
+    params = device_params(prob)
+    a, sa = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype), params=params)
+    b, sb = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype, wavefront=False), params=params)
+    assert sa.last_forward == "wavefront" and sb.last_forward == "layers"
+    assert normwise(a["y"], b["y"]) < 1e-2
+    assert normwise(a["dx"], b["dx"]) < 2e-2
+
+
 def test_deterministic():
     """Two identical runs give bitwise-identical outputs and gradients."""
     wl = small_stack_workload("bf16")
