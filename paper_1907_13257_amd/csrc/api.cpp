@@ -289,17 +289,24 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
             wb[l].cs = reinterpret_cast<float *>(rv + hs[l]->r_cs);
             wb[l].y = y[l];
         }
-        // layer 0's input projection as in lstm_forward; the others are computed in the wavefront
-        GemmDesc g{};
-        g.in = DType::BF16; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
-        g.M = (int)h0->TB; g.N = (int)h0->G4; g.K = d0.I;
-        g.A = x; g.lda = h0->ldx;
-        g.B = W[0]; g.ldb = d0.I;
-        g.C = wb[0].gates; g.ldc = h0->G4;
-        g.bias = b[0]; g.beta = 0;
-        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+        // Layer 0's input projection: inside the wavefront when x has the
+        // layers' width (an otherwise idle XCD computes it step by step),
+        // else by the GEMM as in lstm_forward.  The other layers' are always
+        // computed in the wavefront.
+        const bool x_in_wave = d0.I == d0.H && h0->ldx == d0.H;
+        if (!x_in_wave) {
+            GemmDesc g{};
+            g.in = DType::BF16; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
+            g.M = (int)h0->TB; g.N = (int)h0->G4; g.K = d0.I;
+            g.A = x; g.lda = h0->ldx;
+            g.B = W[0]; g.ldb = d0.I;
+            g.C = wb[0].gates; g.ldc = h0->G4;
+            g.bias = b[0]; g.beta = 0;
+            TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+        }
         RecShape sh{d0.T, d0.B, d0.I, d0.H, 0, 0, h0->ldy};
-        TRY_HIP("layer wavefront", launch_forward_wave(sh, L, wb, reinterpret_cast<unsigned *>(wv + h0->w_sync),
+        TRY_HIP("layer wavefront", launch_forward_wave(sh, L, x_in_wave ? x : nullptr, wb,
+                                                       reinterpret_cast<unsigned *>(wv + h0->w_sync),
                                                        watchdog_ticks(), s));
         return LSTM_OK;
     } catch (...) {

@@ -214,10 +214,11 @@ unsigned long long watchdog_ticks();
 // side job) already did.
 constexpr uint16_t XCD_NOT_READY = 0xffffu;
 // Layer wavefront forward of a stack of L (2..4) unidirectional bf16 layers
-// (H = 1024, at most 16 batch rows, zero initial states, y dense): layer 0's
-// input projection must already be in ly[0].gates (with bias); layers >= 1
-// take their input from the layer below.  Fills the exchanged rows and the
-// flags itself.
+// (H = 1024, at most 16 batch rows, zero initial states, y dense): with x
+// NULL, layer 0's input projection must already be in ly[0].gates (with
+// bias); with x given ([T][B][H], dense), the launch computes it.  Layers
+// >= 1 take their input from the layer below.  Fills the exchanged rows and
+// the flags itself.
 struct WaveBufs {
     const void *R, *W;
     const float *bias;
@@ -225,7 +226,7 @@ struct WaveBufs {
     void *y;
 };
 bool wave_path_ok(const RecShape &sh, int num_cus);
-hipError_t launch_forward_wave(const RecShape &sh, int L, const WaveBufs *ly, unsigned *sync,
+hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
                                unsigned long long timeout, hipStream_t s);
 SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
 SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);

@@ -378,7 +378,10 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 // into the recurrence) are stored with device-coherent (sc1) stores and read
 // with sc1 loads under the NOT_READY protocol: y is filled with the bf16
 // pattern, the projections of layers >= 1 with the fp32 pattern 0xffffffff,
-// before the launch.  Layer 0's projection comes from the GEMM as usual.
+// before the launch.  Layer 0's projection is either given (computed by the
+// GEMM before the launch) or computed on XCD 1 from the stack's input x when
+// its width is H (x is complete at the launch, so it is read without the
+// protocol).
 struct WaveLayer {
     const bf16_t *R, *W;
     const float *bias;
@@ -388,6 +391,7 @@ struct WaveLayer {
 
 struct XWaveArgs {
     int T, B, H, L;
+    const bf16_t *x;     // the stack's input [T][B][H] when XCD 1 projects it; NULL: layer 0's projection is given
     WaveLayer ly[4];
     unsigned *flags;
     unsigned long long timeout;
@@ -419,7 +423,7 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     if (!claim_role(a.flags, &s_xcd)) return;
     const int xcd = s_xcd, layer = xcd >> 1;
     const bool wrole = (xcd & 1) != 0;
-    if (layer >= a.L || (wrole && layer == 0)) return;
+    if (layer >= a.L || (wrole && layer == 0 && !a.x)) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, slot = blockIdx.x >> 3;
     const int H = a.H, B = a.B;
     const long G4 = 4L * H;
@@ -450,8 +454,9 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     if (tid == 0) s_bad = 0;   // ordered by the first barrier below
 
     if (wrole) {
-        // input projection of layer l from the rows of y_{l-1}
-        const u32x4 rs_x = buffer_desc(a.ly[layer - 1].y, (long)a.T * B * H * 2);
+        // input projection of layer l from the rows of y_{l-1} (of x for layer 0)
+        const bool from_x = layer == 0;
+        const u32x4 rs_x = buffer_desc(from_x ? a.x : a.ly[layer - 1].y, (long)a.T * B * H * 2);
         float bz[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) bz[g] = has_cell ? ly.bias[g * H + cj] : 0.0f;
@@ -459,9 +464,20 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
             f32x4 acc[NB];
 #pragma unroll
             for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B, H, w * KW * 2, tile, stage[w], lane, B,
-                                                         rf, acc, a.flags, a.timeout, slot))
+            if (from_x) {
+                if (s > 0) wait_own_lds();   // the previous step's fragment reads are done
+                stage_rows<RB>(rs_x, (long)s * B, H, w * KW * 2, tile, lane);
+                wait_own_loads();
+#pragma unroll
+                for (int c = 0; c < KCW; ++c) {
+                    const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
+#pragma unroll
+                    for (int i = 0; i < NB; ++i) mfma16(acc[i], rf[i][c], fa, bf16_t{});
+                }
+            } else if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B, H, w * KW * 2, tile, stage[w], lane,
+                                                                B, rf, acc, a.flags, a.timeout, slot)) {
                 s_bad = 1;
+            }
 #pragma unroll
             for (int i = 0; i < NB; ++i)
                 *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
@@ -490,7 +506,7 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     const __amdgpu_buffer_rsrc_t ryw =
         __builtin_amdgcn_make_buffer_rsrc(ly.y, (short)0, (int)((long)a.T * B * H * 2), 0x00020000);
     const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
-    const bool poll_gx = layer > 0;
+    const bool poll_gx = layer > 0 || a.x != nullptr;
     float creg = 0.0f;
     for (int s = 0; s < a.T; ++s) {
         // this step's input projection (layers > 0: may still be in flight)
@@ -803,18 +819,44 @@ bool xcd_path_ok(DType t, const RecShape &sh, int num_cus)
 
 void xcd_path_disable() { g_xcd_disabled = 1; }
 
+namespace {
+// Up to 9 word ranges filled with a value each, one launch: range r is
+// handled by the workgroups with blockIdx.y == r, 16-byte stores where the
+// range allows them.
+struct FillRanges {
+    uint32_t *p[9];
+    long n[9];
+    uint32_t v[9];
+};
+
+__global__ __launch_bounds__(256) void fill_ranges_kernel(FillRanges f)
+{
+    const int r = blockIdx.y;
+    uint32_t *p = f.p[r];
+    const long n = f.n[r];
+    const uint32_t v = f.v[r];
+    const long stride = (long)gridDim.x * 256;
+    const bool vec = (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+    const long nv = vec ? n / 4 : 0;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < nv; i += stride)
+        reinterpret_cast<u32x4 *>(p)[i] = u32x4{v, v, v, v};
+    for (long i = nv * 4 + (long)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+}  // namespace
+
 bool wave_path_ok(const RecShape &sh, int num_cus)
 {
     return !g_xcd_disabled && num_cus == NXCD * WG_PER_XCD && sh.H == 1024 && sh.Hp == 0 && sh.reverse == 0 &&
            sh.B >= 1 && sh.B <= 16 && sh.ldy == sh.H && (long)sh.T * sh.B * 4L * sh.H * 4 <= 0x7fffffffL;
 }
 
-hipError_t launch_forward_wave(const RecShape &sh, int L, const WaveBufs *ly, unsigned *sync,
+hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
                                unsigned long long timeout, hipStream_t s)
 {
     if (L < 2 || L > 4) return hipErrorInvalidValue;
     XWaveArgs a{};
     a.T = sh.T; a.B = sh.B; a.H = sh.H; a.L = L;
+    a.x = static_cast<const bf16_t *>(x);
     for (int l = 0; l < L; ++l) {
         a.ly[l].R = static_cast<const bf16_t *>(ly[l].R);
         a.ly[l].W = static_cast<const bf16_t *>(ly[l].W);
@@ -825,19 +867,35 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const WaveBufs *ly, un
     }
     a.flags = sync + XCD_FLAGS;
     a.timeout = timeout;
-    hipError_t e = fill_u32(a.flags, XCD_WORDS, 0u, s);
+    // every exchanged row waits for its producer: y of each layer (dense, two
+    // NOT_READY halves per word), and the input projections that the
+    // projection XCDs write; the flags start at zero
     const long rows = (long)sh.T * sh.B;
-    for (int l = 0; l < L && e == hipSuccess; ++l) {
-        // every exchanged row waits for its producer: y of each layer, and
-        // the input projections that the projection XCDs write
-        e = fill_rows_u16(ly[l].y, rows, sh.H, sh.H, NOT_READY, s);
-        if (e == hipSuccess && l > 0) e = fill_u32(ly[l].gates, (size_t)rows * 4 * sh.H, NOT_READY_F32, s);
+    FillRanges f{};
+    int nr = 0;
+    f.p[nr] = a.flags; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
+    for (int l = 0; l < L; ++l) {
+        f.p[nr] = static_cast<uint32_t *>(ly[l].y); f.n[nr] = rows * sh.H / 2;
+        f.v[nr++] = ((uint32_t)NOT_READY << 16) | NOT_READY;
+        if (l > 0 || x) {
+            f.p[nr] = reinterpret_cast<uint32_t *>(ly[l].gates); f.n[nr] = rows * 4 * sh.H;
+            f.v[nr++] = NOT_READY_F32;
+        }
+    }
+    hipError_t e;
+    {
+        double bytes = 0.0;
+        for (int r = 0; r < nr; ++r) bytes += 4.0 * f.n[r];
+        ProfScope pf(K_SMALL, s, 0.0, bytes);
+        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, nr), dim3(256), 0, s, f);
+        e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
-    ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (2 * L - 1),
+    const int np = x ? L : L - 1;   // input projections computed in the launch
+    ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + np),
                  (double)L * (sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0) +
-                     (L - 1) * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
+                     np * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
     return launch256<lstm_fwd_wave<32>>(s, &a);
 }
 
