@@ -135,6 +135,34 @@ lstm_status_t lstm_backward(lstm_handle_t h,
                             float *dW, float *dR, float *db, float *dP,
                             int accumulate, void *workspace, void *stream);
 
+/* Backward pass of a stack run forward by lstm_forward_stack, as a layer
+ * wavefront: layer l-1's BPTT step t starts as soon as layer l has produced
+ * dz_{l,t} and its input gradient dx_{l,t} = dz_{l,t} W_l (the upstream
+ * gradient of layer l-1), so the layers' BPTT runs a few steps apart instead
+ * of one after another; the weight gradients follow per layer.  The result
+ * equals lstm_backward on each layer from the top down, with dy of layer l-1
+ * = dx of layer l, zero initial states and no gradient for the final states.
+ *   h[l], W[l], R[l], y[l], reserve[l]: as given to lstm_forward_stack
+ *     (every layer with I = H: the stack's input x has the layers' width).
+ *   dy: gradient of the top layer's output y[L-1], [T][B][H].
+ *   x: the stack's input (layer 0's input).
+ *   dx: gradient of x [T][B][H], NULL when not wanted.
+ *   dW[l], dR[l], db[l]: fp32 weight gradients of layer l; accumulate as for
+ *     lstm_backward.
+ *   workspace: lstm_backward_stack_workspace_size(L, h) bytes (per-layer R^T,
+ *     W^T and dz, and the gradients passed between layers).
+ * Runs when L is 2..4, T >= 2, H = 1024 and B <= 16 on an MI355X whose
+ * XCD-local path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the
+ * caller runs lstm_backward layer by layer. */
+lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *h, const void *dy, const void *x,
+                                  const void *const *W, const void *const *R, const void *const *y,
+                                  const void *const *reserve, void *dx, float *const *dW, float *const *dR,
+                                  float *const *db, int accumulate, void *workspace, void *stream);
+
+/* Workspace bytes lstm_backward_stack needs for these layers; 0 when the
+ * stack's shapes do not fit the backward layer wavefront. */
+size_t lstm_backward_stack_workspace_size(int L, const lstm_handle_t *h);
+
 /* Environment: LSTM355_XCD_LAUNCH=cooperative makes the persistent
  * recurrence kernels of the bf16 path wait, as cooperative launches, until
  * all their workgroups (one per CU) can be resident.  By default they are

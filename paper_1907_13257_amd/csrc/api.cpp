@@ -314,6 +314,150 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
     }
 }
 
+namespace {
+// Workspace of lstm_backward_stack: flags, then per layer R^T, W^T, dz and
+// (below the top layer) the upstream gradient written inside the launch,
+// then the bias gradients.
+struct StackBwdLayout {
+    size_t sync, rt[4], wt[4], dz[4], dy[4], dbp, total;
+};
+
+StackBwdLayout stack_bwd_layout(int L, const lstm_desc_t &d)
+{
+    StackBwdLayout w{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = align256(off + bytes);
+        return o;
+    };
+    const size_t H = (size_t)d.H, TB = (size_t)d.T * d.B;
+    w.sync = take((size_t)(XCD_FLAGS + XCD_WORDS) * 4);
+    for (int l = 0; l < L; ++l) {
+        w.rt[l] = take(4 * H * H * 2);
+        w.wt[l] = take(4 * H * H * 2);
+        w.dz[l] = take(TB * 4 * H * 2);
+        w.dy[l] = l < L - 1 ? take(TB * H * 2) : 0;
+    }
+    w.dbp = take((size_t)L * 4 * H * 4);
+    w.total = off;
+    return w;
+}
+
+// Descriptor-level conditions of the backward layer wavefront (no device query).
+const char *stack_bwd_unfit(int L, const lstm_handle_t *hs)
+{
+    if (L < 2 || L > 4) return "needs 2 to 4 layers";
+    const lstm_desc_t &d0 = hs[0]->d;
+    if (d0.T < 2) return "needs T >= 2";
+    for (int l = 0; l < L; ++l) {
+        const lstm_desc_t &d = hs[l]->d;
+        if (hs[l]->dt != DType::BF16 || d.Hp != 0 || d.reverse != 0) return "bf16 LSTM layers only";
+        if (d.T != d0.T || d.B != d0.B || d.H != d0.H) return "layers differ in T, B or H";
+        if (d.I != d.H || hs[l]->ldx != d.H || hs[l]->ldy != d.H) return "every layer needs I = H and dense x, y";
+    }
+    return nullptr;
+}
+}  // namespace
+
+extern "C" size_t lstm_backward_stack_workspace_size(int L, const lstm_handle_t *hs)
+{
+    if (!hs || L < 1) return 0;
+    for (int l = 0; l < L; ++l)
+        if (!hs[l]) return 0;
+    if (stack_bwd_unfit(L, hs)) return 0;
+    return stack_bwd_layout(L, hs[0]->d).total;
+}
+
+extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, const void *dy, const void *x,
+                                             const void *const *W, const void *const *R, const void *const *y,
+                                             const void *const *reserve, void *dx, float *const *dW,
+                                             float *const *dR, float *const *db, int accumulate, void *workspace,
+                                             void *stream)
+{
+    try {
+        if (L < 1 || !hs || !dy || !x || !W || !R || !y || !reserve || !dW || !dR || !db || !workspace)
+            return invalid("required pointer is NULL or L < 1");
+        if (accumulate != 0 && accumulate != 1) return invalid("accumulate must be 0 or 1");
+        for (int l = 0; l < L; ++l) {
+            if (!hs[l] || !W[l] || !R[l] || !y[l] || !reserve[l] || !dW[l] || !dR[l] || !db[l])
+                return invalid("required pointer is NULL");
+            for (const void *p : {W[l], R[l], y[l], reserve[l]})
+                if (!aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+            for (const void *p : {(const void *)dW[l], (const void *)dR[l], (const void *)db[l]})
+                if (!aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+        }
+        for (const void *p : {dy, x, (const void *)dx, (const void *)workspace})
+            if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+        if (const char *why = stack_bwd_unfit(L, hs)) {
+            std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: %s", why);
+            return LSTM_ERR_UNSUPPORTED;
+        }
+        const lstm_desc_t &d0 = hs[0]->d;
+        const int T = d0.T, B = d0.B, H = d0.H;
+        const long G4 = 4L * H, TB = (long)T * B;
+        for (int l = 0; l < L; ++l) {   // the checks that query the device
+            lstm_status_t st = ensure_plan(hs[l]);
+            if (st != LSTM_OK) return st;
+            RecShape sh{T, B, H, H, 0, 0, hs[l]->ldy};
+            if (!wave_path_ok(sh, hs[l]->num_cus)) {
+                std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: shape or device");
+                return LSTM_ERR_UNSUPPORTED;
+            }
+        }
+        const StackBwdLayout lay = stack_bwd_layout(L, d0);
+        char *wv = static_cast<char *>(workspace);
+        // [dW | dR] of every layer as one product each (checked before anything runs)
+        GemmDesc gw[4];
+        for (int l = 0; l < L; ++l) {
+            GemmDesc &g = gw[l];
+            g = GemmDesc{};
+            g.in = DType::BF16; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
+            g.M = (int)G4; g.N = 2 * H; g.K = (int)TB;
+            g.A = wv + lay.dz[l]; g.lda = G4;
+            g.B = l == 0 ? x : y[l - 1]; g.ldb = H;
+            g.C = dW[l]; g.ldc = H; g.beta = accumulate;
+            g.N1 = H;
+            g.B2 = y[l]; g.ldb2 = H; g.b2_bytes = TB * H * 2;   // dz_t pairs with y_{t-1}; h0 is zero
+            g.ylo = B; g.yhi = (int)TB; g.yoff = -B; g.hlo = 0; g.hlen = B;
+            g.C2 = dR[l]; g.ldc2 = H;
+            g.side.sum_src = reinterpret_cast<const float *>(wv + lay.dbp) + (size_t)l * G4;
+            g.side.sum_rows = 1;
+            g.side.sum_cols = (int)G4;
+            g.side.sum_dst = db[l];
+            g.side.sum_acc = accumulate;
+            if (!gemm_dual_ok(g)) {
+                std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: weight-gradient shape");
+                return LSTM_ERR_UNSUPPORTED;
+            }
+        }
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        WaveBwdBufs wb[4];
+        for (int l = 0; l < L; ++l) {
+            const char *rv = static_cast<const char *>(reserve[l]);
+            const bool want_dx = l > 0 || dx;
+            TRY_HIP("transpose R", transpose(DType::BF16, R[l], (int)G4, H, wv + lay.rt[l], s));
+            if (want_dx) TRY_HIP("transpose W", transpose(DType::BF16, W[l], (int)G4, H, wv + lay.wt[l], s));
+            wb[l].Rt = wv + lay.rt[l];
+            wb[l].Wt = want_dx ? wv + lay.wt[l] : nullptr;
+            wb[l].gates = reinterpret_cast<const float *>(rv + hs[l]->r_gates);
+            wb[l].cs = reinterpret_cast<const float *>(rv + hs[l]->r_cs);
+            wb[l].dz = wv + lay.dz[l];
+            wb[l].dy = l == L - 1 ? dy : wv + lay.dy[l];
+            wb[l].dy_fill = l == L - 1 ? nullptr : wv + lay.dy[l];
+            wb[l].dx = l == 0 ? dx : wv + lay.dy[l - 1];
+            wb[l].dbp = reinterpret_cast<float *>(wv + lay.dbp) + (size_t)l * G4;
+        }
+        RecShape sh{T, B, H, H, 0, 0, hs[0]->ldy};
+        TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, reinterpret_cast<unsigned *>(wv + lay.sync),
+                                                                   watchdog_ticks(), s));
+        for (int l = 0; l < L; ++l) TRY_HIP("dW|dR", gemm(gw[l], s, K_GEMM_DWR));
+        return LSTM_OK;
+    } catch (...) {
+        return invalid("exception");
+    }
+}
+
 extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const void *dhT, const float *dcT,
                                        const void *x, const void *h0, const float *c0, const void *W, const void *R,
                                        const void *P, const void *y, const void *reserve, void *dx, void *dh0,

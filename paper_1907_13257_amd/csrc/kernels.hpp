@@ -228,6 +228,22 @@ struct WaveBufs {
 bool wave_path_ok(const RecShape &sh, int num_cus);
 hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
                                unsigned long long timeout, hipStream_t s);
+// Backward of the layer wavefront (I = H = 1024 for every layer): Rt, Wt are
+// R^T and W^T [H][4H] (Wt NULL: no input gradient for that layer); dz
+// [T][B][4H] per layer; dy the upstream gradient (the stack's for the top
+// layer, else the dx of the layer above, which this launch writes: dy_fill
+// is the same buffer, armed before the launch); dbp [4H] the bias gradient.
+struct WaveBwdBufs {
+    const void *Rt, *Wt;
+    const float *gates, *cs;
+    void *dz;
+    const void *dy;
+    void *dy_fill;   // dy when the launch writes it (layers below the top), else NULL
+    void *dx;
+    float *dbp;
+};
+hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
+                                unsigned long long timeout, hipStream_t s);
 SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
 SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);
 hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s,

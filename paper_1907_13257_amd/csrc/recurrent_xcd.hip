@@ -582,6 +582,201 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     }
 }
 
+// Backward of the layer wavefront (stacks of 2..4 layers with I = H = 1024,
+// at most 16 batch rows): XCD 2l runs layer l's BPTT with the rows of R_l^T
+// resident and stores dz_l; XCD 2l+1 multiplies each step's dz_{l,t} by W_l
+// (the rows of W_l^T resident) into dx_{l,t}, which is the upstream gradient
+// dy_{l-1,t} of layer l-1 (for l = 0 the stack's input gradient).  Layer
+// l-1's BPTT thus follows layer l's a few steps behind.  dz and the dy rows
+// that cross XCDs are stored with sc1 stores and read with sc1 loads under
+// the NOT_READY protocol (both filled before the launch).
+struct WaveBwdLayer {
+    const bf16_t *Rt, *Wt;     // [H][4H]: R_l^T, W_l^T (Wt NULL: no input gradient wanted)
+    const float *gates, *cs;   // activations and cell states saved by the forward
+    bf16_t *dz;                // [T][B][4H]
+    const bf16_t *dy;          // [T][B][H] upstream gradient (for l < L-1 written by XCD 2l+3)
+    bf16_t *dx;                // [T][B][H] input gradient (dy of layer l-1, or the stack's dx)
+    float *dbp;                // [4H] bias gradient of layer l
+};
+
+struct XWaveBwdArgs {
+    int T, B, H, L;
+    WaveBwdLayer ly[4];
+    unsigned *flags;
+    unsigned long long timeout;
+};
+
+template <int HN>
+__global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
+{
+    constexpr int NBB = HN / 16;
+    constexpr int NC = 16 * NBB;
+    constexpr int KW = 16 * HN;                   // k per wave (4H / 8)
+    constexpr int KCW = KW / 32;
+    constexpr int RB = KW * 2;
+    constexpr int NCELL = 16 * HN;
+    constexpr int RP = NC + 4;
+    __shared__ float red[8][16][RP];
+    __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
+    __shared__ int s_xcd;
+    __shared__ int s_bad;
+
+    if (!claim_role(a.flags, &s_xcd)) return;
+    const int xcd = s_xcd, layer = xcd >> 1;
+    const bool xrole = (xcd & 1) != 0;
+    if (layer >= a.L) return;
+    const WaveBwdLayer ly = a.ly[layer];
+    if (xrole && !ly.Wt) return;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, slot = blockIdx.x >> 3;
+    const int H = a.H, B = a.B, T = a.T;
+    const long G4 = 4L * H;
+    const int j0 = slot * HN;
+    const unsigned tile = lds_addr(&stage[w][0]);
+
+    // resident: rows j0.. of R_l^T (BPTT) or W_l^T (input gradient), this wave's k range
+    const bf16_t *Mt = xrole ? ly.Wt : ly.Rt;
+    u32x4 rf[NBB][KCW];
+#pragma unroll
+    for (int i = 0; i < NBB; ++i) {
+        const bf16_t *rrow = Mt + (long)(j0 + i * 16 + (lane & 15)) * G4 + w * KW;
+#pragma unroll
+        for (int c = 0; c < KCW; ++c) rf[i][c] = ldg16(rrow + c * 32 + (lane >> 4) * 8);
+    }
+    const u32x4 rs_dz = buffer_desc(ly.dz, (long)T * B * G4 * 2);
+    const bool has_cell = tid < NCELL;
+    const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
+    const int crr = has_cell ? cr : 0;
+    const bool vrow = has_cell && cr < B;
+    if (tid == 0) s_bad = 0;   // ordered by the first barrier below
+
+    if (xrole) {
+        const __amdgpu_buffer_rsrc_t rdx =
+            __builtin_amdgcn_make_buffer_rsrc(ly.dx, (short)0, (int)((long)T * B * H * 2), 0x00020000);
+        for (int s = T - 1; s >= 0; --s) {
+            f32x4 acc[NBB];
+#pragma unroll
+            for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B, G4, w * KW * 2, tile, stage[w], lane, B, rf,
+                                                    acc, a.flags, a.timeout, slot))
+                s_bad = 1;
+#pragma unroll
+            for (int i = 0; i < NBB; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+            __syncthreads();
+            if (s_bad) return;
+            if (vrow) {
+                float v = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+                __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(v)), rdx,
+                                                      (unsigned)((((long)s * B + cr) * H + cj) * 2), 0, 16);
+            }
+            __syncthreads();   // red is rewritten by the next step
+        }
+        return;
+    }
+
+    // BPTT of layer l
+    const __amdgpu_buffer_rsrc_t rdzw =
+        __builtin_amdgcn_make_buffer_rsrc(ly.dz, (short)0, (int)((long)T * B * G4 * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rdy =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t *>(ly.dy), (short)0, (int)((long)T * B * H * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
+    const bool poll_dy = layer < a.L - 1;
+    float dhn = 0.0f, dcn = 0.0f;
+    float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
+    bf16_t dyv;
+    float gv[4], cv, cpv;
+    auto load_inputs = [&](int s) {
+        const unsigned doff = (unsigned)((((long)s * B + crr) * H + cj) * 2);
+        dyv = poll_dy ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16)
+                      : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 0);
+        const long rt = (long)s * B + (vrow ? cr : 0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) gv[g] = vrow ? ly.gates[rt * G4 + g * H + cj] : 0.0f;
+        cv = vrow ? ly.cs[rt * H + cj] : 0.0f;
+        cpv = (vrow && s > 0) ? ly.cs[(rt - B) * H + cj] : 0.0f;
+    };
+    load_inputs(T - 1);
+    for (int s = T - 1; s >= 0; --s) {
+        if (poll_dy) {   // the upstream gradient of this step may still be in flight
+            const unsigned doff = (unsigned)((((long)s * B + crr) * H + cj) * 2);
+            const unsigned long long t0 = wall_clock64();
+            while (__builtin_amdgcn_ballot_w64(vrow && dyv == NOT_READY) != 0) {
+                const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+                if (ab != 0 || wall_clock64() - t0 > a.timeout) {
+                    if (lane == 0 && ab == 0) {
+                        __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    s_bad = 1;
+                    break;
+                }
+                if (vrow && dyv == NOT_READY) dyv = (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16);
+            }
+        }
+        // gate gradients of the owned cells (every lane computes, only the stores depend on the lane)
+        {
+            const float ig = gv[0], fg = gv[1], gg = gv[2], og = gv[3];
+            const float dm = to_f32(dyv) + dhn;
+            const float tc = tanh_f(cv);
+            const float d_o = dm * tc;
+            const float d_c = dcn + dm * og * (1.0f - tc * tc);
+            const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv;
+            const float z[4] = {d_i * ig * (1.0f - ig), d_f * fg * (1.0f - fg), d_g * (1.0f - gg * gg),
+                                d_o * og * (1.0f - og)};
+            if (vrow) {
+                const unsigned zoff = (unsigned)((((long)s * B + cr) * G4 + cj) * 2);
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(z[g])), rdzw,
+                                                          zoff + (unsigned)(g * H * 2), 0, 16);
+            }
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dbacc[g] += vrow ? z[g] : 0.0f;
+            dcn = d_c * fg;
+        }
+        if (s == 0) break;
+        load_inputs(s - 1);
+        f32x4 acc[NBB];
+#pragma unroll
+        for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B, G4, w * KW * 2, tile, stage[w], lane, B, rf, acc,
+                                                a.flags, a.timeout, slot))
+            s_bad = 1;
+#pragma unroll
+        for (int i = 0; i < NBB; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+        __syncthreads();
+        if (s_bad) return;
+        if (vrow) {
+            float v = 0.0f;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+            dhn = v;
+        }
+        __syncthreads();
+    }
+    // bias gradient of layer l: sum this workgroup's rows (in row order)
+    {
+        float *dred = &red[0][0][0];                  // 16 x HN x 4 floats fit in red
+        __syncthreads();
+        if (has_cell) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dred[(cr * HN + cu) * 4 + g] = dbacc[g];
+        }
+        __syncthreads();
+        if (tid < 4 * HN) {
+            const int g = tid / HN, u = tid % HN;
+            float v = 0.0f;
+            for (int r = 0; r < 16; ++r) v += dred[(r * HN + u) * 4 + g];
+            ly.dbp[g * H + j0 + u] = v;
+        }
+    }
+}
+
 struct XBwdArgs {
     int T, B, H, reverse, RX;
     long ldy;
@@ -897,6 +1092,53 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
                  (double)L * (sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0) +
                      np * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
     return launch256<lstm_fwd_wave<32>>(s, &a);
+}
+
+hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
+                                unsigned long long timeout, hipStream_t s)
+{
+    if (L < 2 || L > 4) return hipErrorInvalidValue;
+    XWaveBwdArgs a{};
+    a.T = sh.T; a.B = sh.B; a.H = sh.H; a.L = L;
+    for (int l = 0; l < L; ++l) {
+        a.ly[l].Rt = static_cast<const bf16_t *>(ly[l].Rt);
+        a.ly[l].Wt = static_cast<const bf16_t *>(ly[l].Wt);
+        a.ly[l].gates = ly[l].gates;
+        a.ly[l].cs = ly[l].cs;
+        a.ly[l].dz = static_cast<bf16_t *>(ly[l].dz);
+        a.ly[l].dy = static_cast<const bf16_t *>(ly[l].dy);
+        a.ly[l].dx = static_cast<bf16_t *>(ly[l].dx);
+        a.ly[l].dbp = ly[l].dbp;
+    }
+    a.flags = sync + XCD_FLAGS;
+    a.timeout = timeout;
+    // dz of every layer and the upstream gradients written inside the launch
+    // wait for their producers; the flags start at zero
+    const long rows = (long)sh.T * sh.B;
+    const uint32_t nr2 = ((uint32_t)NOT_READY << 16) | NOT_READY;
+    FillRanges f{};
+    int nr = 0;
+    f.p[nr] = a.flags; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
+    for (int l = 0; l < L; ++l) {
+        f.p[nr] = static_cast<uint32_t *>(ly[l].dz); f.n[nr] = rows * 4 * sh.H / 2; f.v[nr++] = nr2;
+        if (l > 0) { f.p[nr] = static_cast<uint32_t *>(ly[l - 1].dy_fill); f.n[nr] = rows * sh.H / 2; f.v[nr++] = nr2; }
+    }
+    hipError_t e;
+    {
+        double bytes = 0.0;
+        for (int r = 0; r < nr; ++r) bytes += 4.0 * f.n[r];
+        ProfScope pf(K_SMALL, s, 0.0, bytes);
+        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, nr), dim3(256), 0, s, f);
+        e = hipGetLastError();
+    }
+    if (e != hipSuccess) return e;
+    const double G4 = 4.0 * sh.H;
+    int nx = 0;
+    for (int l = 0; l < L; ++l) nx += ly[l].Wt ? 1 : 0;
+    ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + nx),
+                 (double)L * (sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0) +
+                     nx * ((double)sh.T * sh.B * (G4 * 2.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
+    return launch256<lstm_bwd_wave<32>>(s, &a);
 }
 
 hipError_t xcd_tripped_read_and_clear(unsigned *tripped)

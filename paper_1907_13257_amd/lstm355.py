@@ -58,6 +58,8 @@ def load_library():
         "lstm_forward": ([H] + [vp] * 13, i),
         "lstm_backward": ([H] + [vp] * 18 + [i, vp, vp], i),
         "lstm_forward_stack": ([i] + [vp] * 9, i),
+        "lstm_backward_stack": ([i] + [vp] * 11 + [i, vp, vp], i),
+        "lstm_backward_stack_workspace_size": ([i, vp], sz),
         "lstm_check": ([H, vp, vp], i),
         "lstm_destroy": ([H], i),
         "lstm_status_string": ([i], ctypes.c_char_p),
@@ -143,6 +145,27 @@ def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=N
     if st == LSTM_ERR_UNSUPPORTED:
         return False
     _check(st, "lstm_forward_stack")
+    return True
+
+
+def lstm_backward_stack_workspace_size(handles) -> int:
+    n = len(handles)
+    return load_library().lstm_backward_stack_workspace_size(n, (ctypes.c_void_p * n)(*handles))
+
+
+def lstm_backward_stack(handles, dy, x, Ws, Rs, ys, reserves, dx, dWs, dRs, dbs, accumulate, workspace,
+                        stream=None) -> bool:
+    """Layer-wavefront backward of a stack (lstm_backward_stack).  Returns
+    False when the stack does not fit it (LSTM_ERR_UNSUPPORTED); raises on
+    any other error."""
+    n = len(handles)
+    arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
+    st = load_library().lstm_backward_stack(n, arr(handles), _ptr(dy), _ptr(x), arr(Ws), arr(Rs), arr(ys),
+                                            arr(reserves), _ptr(dx), arr(dWs), arr(dRs), arr(dbs),
+                                            int(bool(accumulate)), _ptr(workspace), _stream(stream))
+    if st == LSTM_ERR_UNSUPPORTED:
+        return False
+    _check(st, "lstm_backward_stack")
     return True
 
 
@@ -275,6 +298,8 @@ class Stack:
         self.T, self.B, self.dtype, self.device = T, B, dtype, device
         self.wavefront = wavefront
         self.last_forward = None
+        self.last_backward = None
+        self.wave_ws = None
         self.layers = list(layers)
         td = torch_dtype(dtype)
         self.dirs: List[List[Layer]] = []
@@ -345,6 +370,24 @@ class Stack:
         return cur
 
     def backward(self, d_out, params, grads, accumulate=False, stream=None):
+        # after a wavefront forward, the backward runs as one too when its
+        # shapes allow (lstm_backward_stack)
+        self.last_backward = "layers"
+        if self.last_forward == "wavefront":
+            lays = [d[0] for d in self.dirs]
+            hs = [l.handle for l in lays]
+            need = lstm_backward_stack_workspace_size(hs)
+            if need:
+                import torch
+                if self.wave_ws is None or self.wave_ws.numel() < need:
+                    self.wave_ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+                dx = self.dxbuf[0][0]
+                if lstm_backward_stack(hs, d_out, self.inputs[0], [p[0]["W"] for p in params],
+                                       [p[0]["R"] for p in params], self.y, [l.reserve for l in lays], dx,
+                                       [g[0]["dW"] for g in grads], [g[0]["dR"] for g in grads],
+                                       [g[0]["db"] for g in grads], accumulate, self.wave_ws, stream):
+                    self.last_backward = "wavefront"
+                    return dx
         g = d_out
         for li in range(len(self.layers) - 1, -1, -1):
             L = self.layers[li]

@@ -115,6 +115,34 @@ def test_forward_stack_validates_before_launch(lib):
         L.lstm_destroy(h)
 
 
+def test_backward_stack_validates_before_launch(lib):
+    import ctypes
+    A = 1 << 20
+    arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
+    hb = [L.lstm_create(6, 8, 1024, 1024, 0, "bf16") for _ in range(3)]
+    size = L.lstm_backward_stack_workspace_size(hb)
+    mat, tb = 4 * 1024 * 1024 * 2, 6 * 8
+    assert size >= 3 * (2 * mat + tb * 4096 * 2) + 2 * tb * 1024 * 2
+    assert L.lstm_backward_stack_workspace_size(hb[:1]) == 0          # one layer
+    h1 = L.lstm_create(1, 8, 1024, 1024, 0, "bf16")
+    assert L.lstm_backward_stack_workspace_size([h1, h1]) == 0         # T = 1
+    hn = L.lstm_create(6, 8, 512, 1024, 0, "bf16")
+    assert L.lstm_backward_stack_workspace_size([hn, hb[0]]) == 0      # layer 0 input narrower than H
+
+    def call(hs, dy=A, acc=0):
+        n = len(hs)
+        p = arr([A] * n)
+        return lib.lstm_backward_stack(n, arr(hs), dy, A, p, p, p, p, None, p, p, p, acc, A, None)
+
+    assert call(hb, dy=None) == L.LSTM_ERR_INVALID_ARG
+    assert call(hb, acc=2) == L.LSTM_ERR_INVALID_ARG
+    assert call(hb, dy=A + 2) == L.LSTM_ERR_INVALID_ARG
+    assert call([hn, hb[0]]) == L.LSTM_ERR_UNSUPPORTED
+    assert call([h1, h1]) == L.LSTM_ERR_UNSUPPORTED
+    for h in hb + [h1, hn]:
+        L.lstm_destroy(h)
+
+
 def test_add_validates(lib):
     assert lib.lstm_add(5, 4, 1 << 20, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG
     assert lib.lstm_add(1, 4, None, 1 << 20, 1 << 20, None) == L.LSTM_ERR_INVALID_ARG

@@ -330,6 +330,8 @@ def test_layer_wavefront_stack_parity(T, B, I0, nl):
     prob = synth.draw(wl)
     gpu, stack = run_stack_gpu(prob)
     assert stack.last_forward == "wavefront"
+    # the backward runs as a wavefront too when every layer has I = H and T >= 2
+    assert stack.last_backward == ("wavefront" if I0 == 1024 and T >= 2 else "layers")
     ref = run_oracle(prob)
     compare(gpu, ref, "bf16", label=wl.name)
 
@@ -347,8 +349,37 @@ def test_layer_wavefront_matches_layer_by_layer():
     a, sa = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype), params=params)
     b, sb = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype, wavefront=False), params=params)
     assert sa.last_forward == "wavefront" and sb.last_forward == "layers"
+    assert sa.last_backward == "wavefront" and sb.last_backward == "layers"
     assert normwise(a["y"], b["y"]) < 1e-2
     assert normwise(a["dx"], b["dx"]) < 2e-2
+    for la, lb in zip(a["layers"], b["layers"]):
+        for k in ("dW", "dR", "db"):
+            assert normwise(la[0][k], lb[0][k]) < 2e-2, k
+
+
+def test_layer_wavefront_backward_accumulates():
+    """accumulate = 1 adds the backward wavefront's weight gradients to the
+    given ones: two passes equal twice one pass."""
+    import torch
+    from paper_1907_13257_amd import Stack
+    from _gpu_helpers import device_params, stack_layers
+    wl = synth.Workload("wave_acc", T=5, B=9, layers=[synth.LayerSpec(1024, 1024) for _ in range(2)],
+                        dtype="bf16", seed=23, w_scale=0.05)
+    announce("layer wavefront backward, accumulate")
+    prob = synth.draw(wl)
+    params = device_params(prob)
+    st = Stack(wl.T, wl.B, stack_layers(wl), wl.dtype)
+    grads = st.alloc_grads(params)
+    x, dy = to_dev(prob.x), to_dev(prob.dy)
+    st.forward(x, params)
+    st.backward(dy, params, grads)
+    once = [{k: v.clone() for k, v in g[0].items()} for g in grads]
+    st.backward(dy, params, grads, accumulate=True)
+    torch.cuda.synchronize()
+    assert st.last_backward == "wavefront"
+    for g1, g2 in zip(once, grads):
+        for k in ("dW", "dR", "db"):
+            assert torch.allclose(g2[0][k], 2 * g1[k], rtol=1e-5, atol=1e-6), k
 
 
 def test_deterministic():
