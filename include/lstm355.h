@@ -106,7 +106,7 @@ lstm_status_t lstm_forward(lstm_handle_t h,
  *   reserve[l]: reserve of layer l (lstm_reserve_size(h[l]) bytes), for
  *     lstm_backward on h[l] exactly as after lstm_forward.
  *   workspace: at least the largest lstm_workspace_size of the handles.
- * Runs when L is 2..4, H = 1024 and B <= 16 on an MI355X whose XCD-local
+ * Runs when L is 2..4, H = 1024 and B <= 32 on an MI355X whose XCD-local
  * path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the caller
  * runs the layers one by one with lstm_forward (which rewrites anything this
  * call may have written). */
@@ -151,7 +151,7 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  *     lstm_backward.
  *   workspace: lstm_backward_stack_workspace_size(L, h) bytes (per-layer R^T,
  *     W^T and dz, and the gradients passed between layers).
- * Runs when L is 2..4, T >= 2, H = 1024 and B <= 16 on an MI355X whose
+ * Runs when L is 2..4, T >= 2, H = 1024 and B <= 32 on an MI355X whose
  * XCD-local path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the
  * caller runs lstm_backward layer by layer. */
 lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *h, const void *dy, const void *x,

@@ -214,7 +214,7 @@ unsigned long long watchdog_ticks();
 // side job) already did.
 constexpr uint16_t XCD_NOT_READY = 0xffffu;
 // Layer wavefront forward of a stack of L (2..4) unidirectional bf16 layers
-// (H = 1024, at most 16 batch rows, zero initial states, y dense): with x
+// (H = 1024, at most 32 batch rows, zero initial states, y dense): with x
 // NULL, layer 0's input projection must already be in ly[0].gates (with
 // bias); with x given ([T][B][H], dense), the launch computes it.  Layers
 // >= 1 take their input from the layer below.  Fills the exchanged rows and

@@ -367,7 +367,7 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 
 // ---------------------------------------------------------------------------
 // Layer wavefront: the forward pass of a stack of L (2..4) unidirectional
-// layers in one launch, for batches of at most 16 rows (all rows in one
+// layers in one launch, for batches of at most 32 rows (all rows in one
 // XCD).  XCD 2l runs layer l's recurrence with the rows of R_l resident, as
 // lstm_fwd_xcd does with all rows in one XCD; XCD 2l+1 (l >= 1) keeps the
 // rows of W_l resident and computes each step's input projection y_{l-1,t}
@@ -405,7 +405,7 @@ __device__ __forceinline__ unsigned ready_f32(float v)
     return u == NOT_READY_F32 ? 0x7fc00000u : u;
 }
 
-template <int HN>
+template <int HN, int MBX>
 __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
 {
     constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
@@ -446,7 +446,6 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
     const int crr = has_cell ? cr : 0;
-    const bool vrow = has_cell && cr < B;
     // bounded descriptors: lanes without a row read rows past the last step
     // at the end (those loads return zero), and no store leaves its tensor
     const __amdgpu_buffer_rsrc_t rg =
@@ -461,42 +460,49 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
 #pragma unroll
         for (int g = 0; g < 4; ++g) bz[g] = has_cell ? ly.bias[g * H + cj] : 0.0f;
         for (int s = 0; s < a.T; ++s) {
-            f32x4 acc[NB];
 #pragma unroll
-            for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (from_x) {
-                if (s > 0) wait_own_lds();   // the previous step's fragment reads are done
-                stage_rows<RB>(rs_x, (long)s * B, H, w * KW * 2, tile, lane);
-                wait_own_loads();
+            for (int mb = 0; mb < MBX; ++mb) {
+                const int rb0 = mb * 16;
+                f32x4 acc[NB];
 #pragma unroll
-                for (int c = 0; c < KCW; ++c) {
-                    const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
+                for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (from_x) {
+                    if (s > 0 || mb > 0) wait_own_lds();   // the previous block's fragment reads are done
+                    stage_rows<RB>(rs_x, (long)s * B + rb0, H, w * KW * 2, tile, lane);
+                    wait_own_loads();
 #pragma unroll
-                    for (int i = 0; i < NB; ++i) mfma16(acc[i], rf[i][c], fa, bf16_t{});
+                    for (int c = 0; c < KCW; ++c) {
+                        const u32x4 fa = stage_frag<RB>(stage[w], c, lane);
+#pragma unroll
+                        for (int i = 0; i < NB; ++i) mfma16(acc[i], rf[i][c], fa, bf16_t{});
+                    }
+                } else {
+                    if (mb > 0) wait_own_lds();
+                    if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B + rb0, H, w * KW * 2, tile,
+                                                                 stage[w], lane, B - rb0, rf, acc, a.flags, a.timeout,
+                                                                 slot))
+                        s_bad = 1;
                 }
-            } else if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B, H, w * KW * 2, tile, stage[w], lane,
-                                                                B, rf, acc, a.flags, a.timeout, slot)) {
-                s_bad = 1;
-            }
 #pragma unroll
-            for (int i = 0; i < NB; ++i)
-                *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
-            __syncthreads();
-            if (s_bad) return;
-            if (vrow) {
-                float z[4] = {bz[0], bz[1], bz[2], bz[3]};
+                for (int i = 0; i < NB; ++i)
+                    *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
+                __syncthreads();
+                if (s_bad) return;
+                if (has_cell && rb0 + cr < B) {
+                    float z[4] = {bz[0], bz[1], bz[2], bz[3]};
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][cr][4 * cu]);
+                    for (int q = 0; q < 8; ++q) {
+                        const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][cr][4 * cu]);
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) z[g] += p[g];
+                        for (int g = 0; g < 4; ++g) z[g] += p[g];
+                    }
+                    const unsigned off = (unsigned)((((long)s * B + rb0 + cr) * G4 + cj) * 4);
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        __builtin_amdgcn_raw_buffer_store_b32(ready_f32(z[g]), rg, off + (unsigned)(g * H * 4), 0, 16);
                 }
-                const unsigned off = (unsigned)((((long)s * B + cr) * G4 + cj) * 4);
-#pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    __builtin_amdgcn_raw_buffer_store_b32(ready_f32(z[g]), rg, off + (unsigned)(g * H * 4), 0, 16);
+                __syncthreads();   // red is rewritten by the next block or step
             }
-            __syncthreads();   // red is rewritten by the next step
         }
         return;
     }
@@ -507,83 +513,98 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
         __builtin_amdgcn_make_buffer_rsrc(ly.y, (short)0, (int)((long)a.T * B * H * 2), 0x00020000);
     const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
     const bool poll_gx = layer > 0 || a.x != nullptr;
-    float creg = 0.0f;
+    float creg[MBX];
+#pragma unroll
+    for (int mb = 0; mb < MBX; ++mb) creg[mb] = 0.0f;
     for (int s = 0; s < a.T; ++s) {
-        // this step's input projection (layers > 0: may still be in flight)
-        const unsigned goff = (unsigned)((((long)s * B + crr) * G4 + cj) * 4);
-        unsigned gxu[4];
+        // this step's input projection (may still be in flight when computed in the launch)
+        unsigned gxu[MBX][4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-            gxu[g] = poll_gx ? __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16)
-                             : __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 0);
-        f32x4 acc[NB];
+        for (int mb = 0; mb < MBX; ++mb) {
+            const unsigned goff = (unsigned)((((long)s * B + mb * 16 + crr) * G4 + cj) * 4);
 #pragma unroll
-        for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (s > 0) {
-            if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_y, (long)(s - 1) * B, H, w * KW * 2, tile, stage[w], lane,
-                                                         B, rf, acc, a.flags, a.timeout, slot))
-                s_bad = 1;
+            for (int g = 0; g < 4; ++g)
+                gxu[mb][g] = poll_gx ? __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16)
+                                     : __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < NB; ++i)
-            *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
-        __syncthreads();
-        if (s_bad) return;
-        if (poll_gx) {   // re-read the elements that still hold NOT_READY
-            const unsigned long long t0 = wall_clock64();
-            while (true) {
-                bool nr = false;
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int rb0 = mb * 16;
+            const bool vrow = has_cell && rb0 + cr < B;
+            f32x4 acc[NB];
 #pragma unroll
-                for (int g = 0; g < 4; ++g) nr = nr || (vrow && gxu[g] == NOT_READY_F32);
-                if (__builtin_amdgcn_ballot_w64(nr) == 0) break;
-                const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
-                if (ab != 0 || wall_clock64() - t0 > a.timeout) {
-                    if (lane == 0 && ab == 0) {
-                        __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
+            for (int i = 0; i < NB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (mb > 0) wait_own_lds();   // the previous block's fragment reads are done
+            if (s > 0) {
+                if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_y, (long)(s - 1) * B + rb0, H, w * KW * 2, tile,
+                                                             stage[w], lane, B - rb0, rf, acc, a.flags, a.timeout,
+                                                             slot))
                     s_bad = 1;
-                    break;
+            }
+#pragma unroll
+            for (int i = 0; i < NB; ++i)
+                *reinterpret_cast<f32x4 *>(&red[w][lane & 15][i * 16 + 4 * (lane >> 4)]) = acc[i];
+            __syncthreads();
+            if (s_bad) return;
+            if (poll_gx) {   // re-read the elements that still hold NOT_READY
+                const unsigned goff = (unsigned)((((long)s * B + rb0 + crr) * G4 + cj) * 4);
+                const unsigned long long t0 = wall_clock64();
+                while (true) {
+                    bool nr = false;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) nr = nr || (vrow && gxu[mb][g] == NOT_READY_F32);
+                    if (__builtin_amdgcn_ballot_w64(nr) == 0) break;
+                    const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+                    if (ab != 0 || wall_clock64() - t0 > a.timeout) {
+                        if (lane == 0 && ab == 0) {
+                            __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                        s_bad = 1;
+                        break;
+                    }
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        if (vrow && gxu[mb][g] == NOT_READY_F32)
+                            gxu[mb][g] = __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16);
                 }
-#pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    if (vrow && gxu[g] == NOT_READY_F32)
-                        gxu[g] = __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16);
             }
+            {
+                float z[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) z[g] = __uint_as_float(gxu[mb][g]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) z[g] += p[g];
+                }
+                const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
+                const float c = fg * creg[mb] + ig * gg;
+                const float m = og * tanh_f(c);
+                creg[mb] = c;
+                if (vrow) {
+                    const long row = (long)s * B + rb0 + cr;
+                    const bf16_t hv = ready_value(f32_to_bf16(m));
+                    __builtin_amdgcn_raw_buffer_store_b16(hv, ryw, (unsigned)((row * H + cj) * 2), 0, 16);
+                    // saved activations for the backward pass (not on the critical path)
+                    float *gp = ly.gates + row * G4 + cj;
+                    gp[0] = ig;
+                    gp[H] = fg;
+                    gp[2 * H] = gg;
+                    gp[3 * H] = og;
+                    ly.cs[row * H + cj] = c;
+                }
+            }
+            __syncthreads();   // red is rewritten by the next block or step
+            if (s_bad) return;
         }
-        {
-            float z[4];
-#pragma unroll
-            for (int g = 0; g < 4; ++g) z[g] = __uint_as_float(gxu[g]);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
-#pragma unroll
-                for (int g = 0; g < 4; ++g) z[g] += p[g];
-            }
-            const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
-            const float c = fg * creg + ig * gg;
-            const float m = og * tanh_f(c);
-            creg = c;
-            if (vrow) {
-                const bf16_t hv = ready_value(f32_to_bf16(m));
-                __builtin_amdgcn_raw_buffer_store_b16(hv, ryw, (unsigned)((((long)s * B + cr) * H + cj) * 2), 0, 16);
-                // saved activations for the backward pass (not on the critical path)
-                float *gp = ly.gates + ((long)s * B + cr) * G4 + cj;
-                gp[0] = ig;
-                gp[H] = fg;
-                gp[2 * H] = gg;
-                gp[3 * H] = og;
-                ly.cs[((long)s * B + cr) * H + cj] = c;
-            }
-        }
-        __syncthreads();   // red is rewritten by the next step
-        if (s_bad) return;
     }
 }
 
 // Backward of the layer wavefront (stacks of 2..4 layers with I = H = 1024,
-// at most 16 batch rows): XCD 2l runs layer l's BPTT with the rows of R_l^T
+// at most 32 batch rows): XCD 2l runs layer l's BPTT with the rows of R_l^T
 // resident and stores dz_l; XCD 2l+1 multiplies each step's dz_{l,t} by W_l
 // (the rows of W_l^T resident) into dx_{l,t}, which is the upstream gradient
 // dy_{l-1,t} of layer l-1 (for l = 0 the stack's input gradient).  Layer
@@ -606,7 +627,7 @@ struct XWaveBwdArgs {
     unsigned long long timeout;
 };
 
-template <int HN>
+template <int HN, int MBX>
 __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
 {
     constexpr int NBB = HN / 16;
@@ -646,33 +667,37 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
     const int crr = has_cell ? cr : 0;
-    const bool vrow = has_cell && cr < B;
     if (tid == 0) s_bad = 0;   // ordered by the first barrier below
 
     if (xrole) {
         const __amdgpu_buffer_rsrc_t rdx =
             __builtin_amdgcn_make_buffer_rsrc(ly.dx, (short)0, (int)((long)T * B * H * 2), 0x00020000);
         for (int s = T - 1; s >= 0; --s) {
-            f32x4 acc[NBB];
 #pragma unroll
-            for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B, G4, w * KW * 2, tile, stage[w], lane, B, rf,
-                                                    acc, a.flags, a.timeout, slot))
-                s_bad = 1;
+            for (int mb = 0; mb < MBX; ++mb) {
+                const int rb0 = mb * 16;
+                f32x4 acc[NBB];
 #pragma unroll
-            for (int i = 0; i < NBB; ++i)
+                for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (mb > 0) wait_own_lds();
+                if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B + rb0, G4, w * KW * 2, tile, stage[w], lane,
+                                                        B - rb0, rf, acc, a.flags, a.timeout, slot))
+                    s_bad = 1;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
-            __syncthreads();
-            if (s_bad) return;
-            if (vrow) {
-                float v = 0.0f;
+                for (int i = 0; i < NBB; ++i)
 #pragma unroll
-                for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
-                __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(v)), rdx,
-                                                      (unsigned)((((long)s * B + cr) * H + cj) * 2), 0, 16);
+                    for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+                __syncthreads();
+                if (s_bad) return;
+                if (has_cell && rb0 + cr < B) {
+                    float v = 0.0f;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+                    __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(v)), rdx,
+                                                          (unsigned)((((long)s * B + rb0 + cr) * H + cj) * 2), 0, 16);
+                }
+                __syncthreads();   // red is rewritten by the next block or step
             }
-            __syncthreads();   // red is rewritten by the next step
         }
         return;
     }
@@ -684,50 +709,60 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
         __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t *>(ly.dy), (short)0, (int)((long)T * B * H * 2), 0x00020000);
     const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
     const bool poll_dy = layer < a.L - 1;
-    float dhn = 0.0f, dcn = 0.0f;
+    float dhn[MBX], dcn[MBX];
     float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
-    bf16_t dyv;
-    float gv[4], cv, cpv;
-    auto load_inputs = [&](int s) {
-        const unsigned doff = (unsigned)((((long)s * B + crr) * H + cj) * 2);
-        dyv = poll_dy ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16)
-                      : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 0);
-        const long rt = (long)s * B + (vrow ? cr : 0);
+    bf16_t dyv[MBX];
+    float gv[MBX][4], cv[MBX], cpv[MBX];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) gv[g] = vrow ? ly.gates[rt * G4 + g * H + cj] : 0.0f;
-        cv = vrow ? ly.cs[rt * H + cj] : 0.0f;
-        cpv = (vrow && s > 0) ? ly.cs[(rt - B) * H + cj] : 0.0f;
+    for (int mb = 0; mb < MBX; ++mb) dhn[mb] = dcn[mb] = 0.0f;
+    auto load_inputs = [&](int s) {
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const bool v = has_cell && mb * 16 + cr < B;
+            const unsigned doff = (unsigned)((((long)s * B + mb * 16 + crr) * H + cj) * 2);
+            dyv[mb] = poll_dy ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16)
+                              : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 0);
+            const long rt = (long)s * B + (v ? mb * 16 + cr : 0);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gv[mb][g] = v ? ly.gates[rt * G4 + g * H + cj] : 0.0f;
+            cv[mb] = v ? ly.cs[rt * H + cj] : 0.0f;
+            cpv[mb] = (v && s > 0) ? ly.cs[(rt - B) * H + cj] : 0.0f;
+        }
     };
     load_inputs(T - 1);
     for (int s = T - 1; s >= 0; --s) {
-        if (poll_dy) {   // the upstream gradient of this step may still be in flight
-            const unsigned doff = (unsigned)((((long)s * B + crr) * H + cj) * 2);
-            const unsigned long long t0 = wall_clock64();
-            while (__builtin_amdgcn_ballot_w64(vrow && dyv == NOT_READY) != 0) {
-                const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
-                if (ab != 0 || wall_clock64() - t0 > a.timeout) {
-                    if (lane == 0 && ab == 0) {
-                        __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int mb = 0; mb < MBX; ++mb) {
+            const bool vrow = has_cell && mb * 16 + cr < B;
+            if (poll_dy) {   // the upstream gradient of this step may still be in flight
+                const unsigned doff = (unsigned)((((long)s * B + mb * 16 + crr) * H + cj) * 2);
+                const unsigned long long t0 = wall_clock64();
+                while (__builtin_amdgcn_ballot_w64(vrow && dyv[mb] == NOT_READY) != 0) {
+                    const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+                    if (ab != 0 || wall_clock64() - t0 > a.timeout) {
+                        if (lane == 0 && ab == 0) {
+                            __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                        s_bad = 1;
+                        break;
                     }
-                    s_bad = 1;
-                    break;
+                    if (vrow && dyv[mb] == NOT_READY)
+                        dyv[mb] = (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16);
                 }
-                if (vrow && dyv == NOT_READY) dyv = (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rdy, doff, 0, 16);
             }
-        }
-        // gate gradients of the owned cells (every lane computes, only the stores depend on the lane)
-        {
-            const float ig = gv[0], fg = gv[1], gg = gv[2], og = gv[3];
-            const float dm = to_f32(dyv) + dhn;
-            const float tc = tanh_f(cv);
+            // gate gradients of the owned cells (every lane computes, only the stores depend on the lane)
+            const float ig = gv[mb][0], fg = gv[mb][1], gg = gv[mb][2], og = gv[mb][3];
+            const float dm = to_f32(dyv[mb]) + dhn[mb];
+            const float tc = tanh_f(cv[mb]);
             const float d_o = dm * tc;
-            const float d_c = dcn + dm * og * (1.0f - tc * tc);
-            const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv;
+            const float d_c = dcn[mb] + dm * og * (1.0f - tc * tc);
+            const float d_i = d_c * gg, d_g = d_c * ig, d_f = d_c * cpv[mb];
             const float z[4] = {d_i * ig * (1.0f - ig), d_f * fg * (1.0f - fg), d_g * (1.0f - gg * gg),
                                 d_o * og * (1.0f - og)};
             if (vrow) {
-                const unsigned zoff = (unsigned)((((long)s * B + cr) * G4 + cj) * 2);
+                const unsigned zoff = (unsigned)((((long)s * B + mb * 16 + cr) * G4 + cj) * 2);
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(z[g])), rdzw,
@@ -735,29 +770,34 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
             }
 #pragma unroll
             for (int g = 0; g < 4; ++g) dbacc[g] += vrow ? z[g] : 0.0f;
-            dcn = d_c * fg;
+            dcn[mb] = d_c * fg;
         }
         if (s == 0) break;
         load_inputs(s - 1);
-        f32x4 acc[NBB];
 #pragma unroll
-        for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B, G4, w * KW * 2, tile, stage[w], lane, B, rf, acc,
-                                                a.flags, a.timeout, slot))
-            s_bad = 1;
+        for (int mb = 0; mb < MBX; ++mb) {
+            const int rb0 = mb * 16;
+            f32x4 acc[NBB];
 #pragma unroll
-        for (int i = 0; i < NBB; ++i)
+            for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (mb > 0) wait_own_lds();
+            if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)s * B + rb0, G4, w * KW * 2, tile, stage[w], lane,
+                                                    B - rb0, rf, acc, a.flags, a.timeout, slot))
+                s_bad = 1;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
-        __syncthreads();
-        if (s_bad) return;
-        if (vrow) {
-            float v = 0.0f;
+            for (int i = 0; i < NBB; ++i)
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
-            dhn = v;
+                for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
+            __syncthreads();
+            if (s_bad) return;
+            if (has_cell && rb0 + cr < B) {
+                float v = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+                dhn[mb] = v;
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
     // bias gradient of layer l: sum this workgroup's rows (in row order)
     {
@@ -1042,7 +1082,7 @@ __global__ __launch_bounds__(256) void fill_ranges_kernel(FillRanges f)
 bool wave_path_ok(const RecShape &sh, int num_cus)
 {
     return !g_xcd_disabled && num_cus == NXCD * WG_PER_XCD && sh.H == 1024 && sh.Hp == 0 && sh.reverse == 0 &&
-           sh.B >= 1 && sh.B <= 16 && sh.ldy == sh.H && (long)sh.T * sh.B * 4L * sh.H * 4 <= 0x7fffffffL;
+           sh.B >= 1 && sh.B <= 32 && sh.ldy == sh.H && (long)sh.T * sh.B * 4L * sh.H * 4 <= 0x7fffffffL;
 }
 
 hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
@@ -1091,7 +1131,8 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + np),
                  (double)L * (sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0) +
                      np * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
-    return launch256<lstm_fwd_wave<32>>(s, &a);
+    if (sh.B <= 16) return launch256<lstm_fwd_wave<32, 1>>(s, &a);
+    return launch256<lstm_fwd_wave<32, 2>>(s, &a);
 }
 
 hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
@@ -1138,7 +1179,8 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + nx),
                  (double)L * (sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0) +
                      nx * ((double)sh.T * sh.B * (G4 * 2.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
-    return launch256<lstm_bwd_wave<32>>(s, &a);
+    if (sh.B <= 16) return launch256<lstm_bwd_wave<32, 1>>(s, &a);
+    return launch256<lstm_bwd_wave<32, 2>>(s, &a);
 }
 
 hipError_t xcd_tripped_read_and_clear(unsigned *tripped)

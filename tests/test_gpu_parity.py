@@ -316,12 +316,14 @@ WAVE_CASES = [
     (5, 5, 512, 3),
     (4, 13, 1024, 4),
     (1, 16, 1024, 2),
+    (5, 32, 1024, 3),      # two row blocks per XCD
+    (4, 20, 1024, 2),      # a ragged second row block
 ]
 
 
 @pytest.mark.parametrize("T,B,I0,nl", WAVE_CASES)
 def test_layer_wavefront_stack_parity(T, B, I0, nl):
-    """A stack of plain layers at B <= 16, H = 1024 runs its forward pass as
+    """A stack of plain layers at B <= 32, H = 1024 runs its forward pass as
     one layer wavefront (lstm_forward_stack); outputs and every gradient of
     the following backward pass match the oracle."""
     layers = [synth.LayerSpec(I0, 1024)] + [synth.LayerSpec(1024, 1024) for _ in range(nl - 1)]
