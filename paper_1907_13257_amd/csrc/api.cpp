@@ -433,11 +433,17 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
         }
         hipStream_t s = static_cast<hipStream_t>(stream);
         WaveBwdBufs wb[4];
+        const void *tsrc[8];
+        void *tdst[8];
+        int nt = 0;
+        for (int l = 0; l < L; ++l) {
+            tsrc[nt] = R[l]; tdst[nt++] = wv + lay.rt[l];
+            if (l > 0 || dx) { tsrc[nt] = W[l]; tdst[nt++] = wv + lay.wt[l]; }
+        }
+        TRY_HIP("transpose R, W", transpose_batch_u16(nt, tsrc, tdst, (int)G4, H, s));   // one launch for all layers
         for (int l = 0; l < L; ++l) {
             const char *rv = static_cast<const char *>(reserve[l]);
             const bool want_dx = l > 0 || dx;
-            TRY_HIP("transpose R", transpose(DType::BF16, R[l], (int)G4, H, wv + lay.rt[l], s));
-            if (want_dx) TRY_HIP("transpose W", transpose(DType::BF16, W[l], (int)G4, H, wv + lay.wt[l], s));
             wb[l].Rt = wv + lay.rt[l];
             wb[l].Wt = want_dx ? wv + lay.wt[l] : nullptr;
             wb[l].gates = reinterpret_cast<const float *>(rv + hs[l]->r_gates);

@@ -108,6 +108,9 @@ bool gemm_dual_ok(const GemmDesc &d);
 // dst[c][r] = src[r][c]; `side` (optional) is done by the same launch.
 hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s,
                      const SideJob *side = nullptr);
+// n (1..8) 16-bit matrices of one shape [rows][cols] (multiples of 64,
+// 16-byte aligned) transposed in one launch.
+hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s);
 hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
 // p[r*ld + c] = v for r < rows, c < cols (16-bit elements).
 hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s);

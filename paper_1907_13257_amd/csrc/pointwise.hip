@@ -27,8 +27,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T *__restrict__ sr
 
 // 16-bit elements, rows and cols multiples of 64, 16-byte aligned: 16-byte
 // loads along the source rows and 16-byte stores along the destination rows.
-__global__ __launch_bounds__(256) void transpose_u16_vec_kernel(const uint16_t *__restrict__ src, int rows, int cols,
-                                                                uint16_t *__restrict__ dst, SideJob side)
+__device__ __forceinline__ void transpose_u16_vec_tile(const uint16_t *__restrict__ src, int rows, int cols,
+                                                       uint16_t *__restrict__ dst)
 {
     __shared__ uint16_t tile[64][72];
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
@@ -49,7 +49,24 @@ __global__ __launch_bounds__(256) void transpose_u16_vec_kernel(const uint16_t *
             w[e] = (unsigned)tile[q * 8 + 2 * e][i] | ((unsigned)tile[q * 8 + 2 * e + 1][i] << 16);
         *reinterpret_cast<u32x4 *>(dst + (long)(c0 + i) * rows + r0 + q * 8) = u32x4{w[0], w[1], w[2], w[3]};
     }
+}
+
+__global__ __launch_bounds__(256) void transpose_u16_vec_kernel(const uint16_t *__restrict__ src, int rows, int cols,
+                                                                uint16_t *__restrict__ dst, SideJob side)
+{
+    transpose_u16_vec_tile(src, rows, cols, dst);
     run_side_job(side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+}
+
+// Several matrices of one shape in one launch: matrix blockIdx.z.
+struct TransposeBatch {
+    const uint16_t *src[8];
+    uint16_t *dst[8];
+};
+
+__global__ __launch_bounds__(256) void transpose_u16_vec_batch_kernel(TransposeBatch b, int rows, int cols)
+{
+    transpose_u16_vec_tile(b.src[blockIdx.z], rows, cols, b.dst[blockIdx.z]);
 }
 
 __global__ void fill_kernel(uint32_t *p, size_t n, uint32_t v)
@@ -337,6 +354,21 @@ hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hi
     else
         hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, static_cast<const float *>(src), rows, cols,
                            static_cast<float *>(dst), sj);
+    return hipGetLastError();
+}
+
+hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s)
+{
+    if (n < 1 || n > 8 || rows % 64 || cols % 64) return hipErrorInvalidValue;
+    TransposeBatch b{};
+    for (int i = 0; i < n; ++i) {
+        if (((reinterpret_cast<uintptr_t>(src[i]) | reinterpret_cast<uintptr_t>(dst[i])) & 15) != 0)
+            return hipErrorInvalidValue;
+        b.src[i] = static_cast<const uint16_t *>(src[i]);
+        b.dst[i] = static_cast<uint16_t *>(dst[i]);
+    }
+    ProfScope ps(K_SMALL, s, 0.0, 4.0 * n * (double)rows * cols);
+    hipLaunchKernelGGL(transpose_u16_vec_batch_kernel, dim3(cols / 64, rows / 64, n), dim3(256), 0, s, b, rows, cols);
     return hipGetLastError();
 }
 
