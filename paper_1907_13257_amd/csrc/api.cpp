@@ -457,7 +457,11 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
         RecShape sh{T, B, H, H, 0, 0, hs[0]->ldy};
         TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, reinterpret_cast<unsigned *>(wv + lay.sync),
                                                                    watchdog_ticks(), s));
-        for (int l = 0; l < L; ++l) TRY_HIP("dW|dR", gemm(gw[l], s, K_GEMM_DWR));
+        // the layers' weight-gradient products as one batched launch
+        GemmDesc gb = gw[0];
+        gb.nbatch = L;
+        gb.batch = gw;
+        TRY_HIP("dW|dR", gemm(gb, s, K_GEMM_DWR));
         return LSTM_OK;
     } catch (...) {
         return invalid("exception");

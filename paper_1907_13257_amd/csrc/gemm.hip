@@ -54,6 +54,14 @@ struct GemmArgs {
     float *cell_c, *cell_cT;
     bf16_t *cell_m;
     long cell_ldm;
+    // batch (blockIdx.z selects the product)
+    int nbatch;
+    struct {
+        const char *A, *B, *B2;
+        char *C, *C2;
+        const float *sum_src;
+        float *sum_dst;
+    } bt[4];
 };
 
 // Global -> register -> LDS staging of one operand for one K stage.
@@ -393,6 +401,17 @@ template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NW
           bool GT = false>
 __global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
 {
+    if (g.nbatch > 1) {   // product blockIdx.z of a batch (product 0's pointers are g's own)
+        // constant indices keep the arguments in scalar registers
+        const int z = blockIdx.z;
+#pragma unroll
+        for (int b = 1; b < 4; ++b)
+            if (z == b) {
+                g.A = g.bt[b].A; g.B = g.bt[b].B; g.B2 = g.bt[b].B2;
+                g.C = g.bt[b].C; g.C2 = g.bt[b].C2;
+                g.side.sum_src = g.bt[b].sum_src; g.side.sum_dst = g.bt[b].sum_dst;
+            }
+    }
     static_assert(!GT || (CB && BKM && BN % 4 == 0), "the cell update accumulates onto C with a k-major B");
     constexpr int NW = NWM * NWN;
     constexpr int WM = BM / NWM, WN = BN / NWN;
@@ -702,6 +721,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
 {
     constexpr int LDS = NS * (BM + BN) * KD * 2;
     GemmArgs g;
+    if (d.nbatch > 1) splits = 1;   // batched products are never split
     g.M = d.M; g.N = d.N; g.K = d.K;
     g.A = static_cast<const char *>(d.A); g.lda = d.lda;
     g.B = static_cast<const char *>(d.B); g.ldb = d.ldb;
@@ -728,7 +748,22 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(64 * NWM * NWN), LDS, s, g);
+    g.nbatch = 1;
+    if (d.nbatch > 1) {
+        if (d.nbatch > 4 || !d.batch) return hipErrorInvalidValue;
+        g.nbatch = d.nbatch;
+        for (int b = 0; b < d.nbatch; ++b) {
+            const GemmDesc &e = d.batch[b];
+            g.bt[b].A = static_cast<const char *>(e.A);
+            g.bt[b].B = static_cast<const char *>(e.B);
+            g.bt[b].B2 = static_cast<const char *>(e.B2);
+            g.bt[b].C = static_cast<char *>(e.C);
+            g.bt[b].C2 = static_cast<char *>(e.C2);
+            g.bt[b].sum_src = e.side.sum_src;
+            g.bt[b].sum_dst = e.side.sum_dst;
+        }
+    }
+    hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits, g.nbatch), dim3(64 * NWM * NWN), LDS, s, g);
     e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     return launch_splitk_reduce<TO>(d, splits, s);
@@ -737,6 +772,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
 template <typename TI, typename TO, int BM, int BN, int KB, bool AK, bool BKM>
 hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
 {
+    if (d.nbatch > 1) return hipErrorInvalidValue;   // batches run on the direct-to-LDS kernel only
     constexpr int KS = KB / (int)sizeof(TI);
     constexpr int LDS = 2 * (BM + BN) * (KB + 16);
     GemmArgs g;
@@ -1099,6 +1135,10 @@ hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
     if (d.cell_h > 0) {   // the cell update's own traffic: read cprev, write activations, c, m
         if (!gemm_cell_ok(d)) return hipErrorInvalidValue;
         bytes += (double)d.M * d.cell_h * (4.0 * (d.cell_prev ? 1 : 0) + 4.0 + 2.0 + (d.cell_cT ? 4.0 : 0.0));
+    }
+    if (d.nbatch > 1) {
+        flops *= d.nbatch;
+        bytes *= d.nbatch;
     }
     ProfScope ps(kclass, s, flops, bytes);
     g_kclass = kclass;

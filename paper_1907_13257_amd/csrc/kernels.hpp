@@ -97,6 +97,13 @@ struct GemmDesc {
     float *cell_c = nullptr;
     void *cell_m = nullptr; long cell_ldm = 0;
     float *cell_cT = nullptr;
+    // Batch: nbatch (<= 4) products of this shape in one launch, batch[i]
+    // giving product i's A, B, B2, C, C2 and side-job sum pointers (the
+    // other fields are this descriptor's).  One product follows another, so
+    // the stores of one overlap the main loop of the next.  Never split
+    // along K.
+    int nbatch = 1;
+    const GemmDesc *batch = nullptr;
 };
 // Whether `gemm` can run the fused cell update for descriptor d.
 bool gemm_cell_ok(const GemmDesc &d);
