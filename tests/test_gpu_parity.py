@@ -318,6 +318,7 @@ WAVE_CASES = [
     (1, 16, 1024, 2),
     (5, 32, 1024, 3),      # two row blocks per XCD
     (4, 20, 1024, 2),      # a ragged second row block
+    (2, 1, 1024, 3),       # the shortest sequence the backward wavefront takes, one batch row
 ]
 
 
@@ -357,6 +358,37 @@ def test_layer_wavefront_matches_layer_by_layer():
     for la, lb in zip(a["layers"], b["layers"]):
         for k in ("dW", "dR", "db"):
             assert normwise(la[0][k], lb[0][k]) < 2e-2, k
+
+
+def test_layer_wavefront_backward_without_input_gradient():
+    """lstm_backward_stack with dx = NULL (layer 0's input-gradient XCD stays
+    idle) gives the same weight gradients as with dx."""
+    import torch
+    from paper_1907_13257_amd import Stack
+    from paper_1907_13257_amd.lstm355 import lstm_backward_stack, lstm_backward_stack_workspace_size
+    from _gpu_helpers import device_params, stack_layers
+    wl = synth.Workload("wave_nodx", T=6, B=12, layers=[synth.LayerSpec(1024, 1024) for _ in range(3)],
+                        dtype="bf16", seed=25, w_scale=0.05)
+    announce("layer wavefront backward without dx")
+    prob = synth.draw(wl)
+    params = device_params(prob)
+    st = Stack(wl.T, wl.B, stack_layers(wl), wl.dtype)
+    grads = st.alloc_grads(params)
+    x, dy = to_dev(prob.x), to_dev(prob.dy)
+    st.forward(x, params)
+    st.backward(dy, params, grads)
+    assert st.last_backward == "wavefront"
+    ref = [{k: v.clone() for k, v in g[0].items()} for g in grads]
+    lays = [d[0] for d in st.dirs]
+    hs = [l.handle for l in lays]
+    ws = torch.empty(lstm_backward_stack_workspace_size(hs), dtype=torch.uint8, device="cuda")
+    assert lstm_backward_stack(hs, dy, x, [p[0]["W"] for p in params], [p[0]["R"] for p in params], st.y,
+                               [l.reserve for l in lays], None, [g[0]["dW"] for g in grads],
+                               [g[0]["dR"] for g in grads], [g[0]["db"] for g in grads], False, ws)
+    torch.cuda.synchronize()
+    for g1, g2 in zip(ref, grads):
+        for k in ("dW", "dR", "db"):
+            assert torch.equal(g1[k], g2[0][k]), k
 
 
 def test_layer_wavefront_backward_accumulates():
