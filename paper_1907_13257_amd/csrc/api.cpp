@@ -440,7 +440,6 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
             tsrc[nt] = R[l]; tdst[nt++] = wv + lay.rt[l];
             if (l > 0 || dx) { tsrc[nt] = W[l]; tdst[nt++] = wv + lay.wt[l]; }
         }
-        TRY_HIP("transpose R, W", transpose_batch_u16(nt, tsrc, tdst, (int)G4, H, s));   // one launch for all layers
         for (int l = 0; l < L; ++l) {
             const char *rv = static_cast<const char *>(reserve[l]);
             const bool want_dx = l > 0 || dx;
@@ -454,9 +453,13 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
             wb[l].dx = l == 0 ? dx : wv + lay.dy[l - 1];
             wb[l].dbp = reinterpret_cast<float *>(wv + lay.dbp) + (size_t)l * G4;
         }
+        // one launch transposes R and W of every layer and arms the rows the
+        // wavefront exchanges; then the wavefront itself
         RecShape sh{T, B, H, H, 0, 0, hs[0]->ldy};
-        TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, reinterpret_cast<unsigned *>(wv + lay.sync),
-                                                                   watchdog_ticks(), s));
+        unsigned *sync = reinterpret_cast<unsigned *>(wv + lay.sync);
+        const FillRanges fills = backward_wave_fills(sh, L, wb, sync);
+        TRY_HIP("transpose R, W", transpose_batch_u16(nt, tsrc, tdst, (int)G4, H, s, &fills));
+        TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, sync, watchdog_ticks(), s, true));
         // the layers' weight-gradient products as one batched launch
         GemmDesc gb = gw[0];
         gb.nbatch = L;

@@ -115,9 +115,18 @@ bool gemm_dual_ok(const GemmDesc &d);
 // dst[c][r] = src[r][c]; `side` (optional) is done by the same launch.
 hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s,
                      const SideJob *side = nullptr);
+// Up to 9 word ranges, each filled with its own value: p[r][0..n[r]) = v[r].
+struct FillRanges {
+    uint32_t *p[9];
+    long n[9];
+    uint32_t v[9];
+    int count;
+};
 // n (1..8) 16-bit matrices of one shape [rows][cols] (multiples of 64,
-// 16-byte aligned) transposed in one launch.
-hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s);
+// 16-byte aligned) transposed in one launch, which also performs `fill`
+// (if given) in slices of its own.
+hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s,
+                               const FillRanges *fill = nullptr);
 hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
 // p[r*ld + c] = v for r < rows, c < cols (16-bit elements).
 hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s);
@@ -252,8 +261,12 @@ struct WaveBwdBufs {
     void *dx;
     float *dbp;
 };
+// The fills launch_backward_wave needs before its launch (flags, dz, the
+// upstream gradients written inside the launch); with `prefilled` the caller
+// has performed them (e.g. inside transpose_batch_u16).
+FillRanges backward_wave_fills(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync);
 hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
-                                unsigned long long timeout, hipStream_t s);
+                                unsigned long long timeout, hipStream_t s, bool prefilled = false);
 SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
 SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);
 hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s,

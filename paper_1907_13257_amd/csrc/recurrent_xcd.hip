@@ -1055,15 +1055,8 @@ bool xcd_path_ok(DType t, const RecShape &sh, int num_cus)
 void xcd_path_disable() { g_xcd_disabled = 1; }
 
 namespace {
-// Up to 9 word ranges filled with a value each, one launch: range r is
-// handled by the workgroups with blockIdx.y == r, 16-byte stores where the
-// range allows them.
-struct FillRanges {
-    uint32_t *p[9];
-    long n[9];
-    uint32_t v[9];
-};
-
+// FillRanges in one launch: range r is handled by the workgroups with
+// blockIdx.y == r, 16-byte stores where the range allows them.
 __global__ __launch_bounds__(256) void fill_ranges_kernel(FillRanges f)
 {
     const int r = blockIdx.y;
@@ -1135,8 +1128,25 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
     return launch256<lstm_fwd_wave<32, 2>>(s, &a);
 }
 
+FillRanges backward_wave_fills(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync)
+{
+    // dz of every layer and the upstream gradients written inside the launch
+    // wait for their producers; the flags start at zero
+    const long rows = (long)sh.T * sh.B;
+    const uint32_t nr2 = ((uint32_t)NOT_READY << 16) | NOT_READY;
+    FillRanges f{};
+    int nr = 0;
+    f.p[nr] = sync + XCD_FLAGS; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
+    for (int l = 0; l < L && l < 4; ++l) {
+        f.p[nr] = static_cast<uint32_t *>(ly[l].dz); f.n[nr] = rows * 4 * sh.H / 2; f.v[nr++] = nr2;
+        if (l > 0) { f.p[nr] = static_cast<uint32_t *>(ly[l - 1].dy_fill); f.n[nr] = rows * sh.H / 2; f.v[nr++] = nr2; }
+    }
+    f.count = nr;
+    return f;
+}
+
 hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
-                                unsigned long long timeout, hipStream_t s)
+                                unsigned long long timeout, hipStream_t s, bool prefilled)
 {
     if (L < 2 || L > 4) return hipErrorInvalidValue;
     XWaveBwdArgs a{};
@@ -1153,26 +1163,15 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
     }
     a.flags = sync + XCD_FLAGS;
     a.timeout = timeout;
-    // dz of every layer and the upstream gradients written inside the launch
-    // wait for their producers; the flags start at zero
-    const long rows = (long)sh.T * sh.B;
-    const uint32_t nr2 = ((uint32_t)NOT_READY << 16) | NOT_READY;
-    FillRanges f{};
-    int nr = 0;
-    f.p[nr] = a.flags; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
-    for (int l = 0; l < L; ++l) {
-        f.p[nr] = static_cast<uint32_t *>(ly[l].dz); f.n[nr] = rows * 4 * sh.H / 2; f.v[nr++] = nr2;
-        if (l > 0) { f.p[nr] = static_cast<uint32_t *>(ly[l - 1].dy_fill); f.n[nr] = rows * sh.H / 2; f.v[nr++] = nr2; }
-    }
-    hipError_t e;
-    {
+    if (!prefilled) {
+        const FillRanges f = backward_wave_fills(sh, L, ly, sync);
         double bytes = 0.0;
-        for (int r = 0; r < nr; ++r) bytes += 4.0 * f.n[r];
+        for (int r = 0; r < f.count; ++r) bytes += 4.0 * f.n[r];
         ProfScope pf(K_SMALL, s, 0.0, bytes);
-        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, nr), dim3(256), 0, s, f);
-        e = hipGetLastError();
+        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, f.count), dim3(256), 0, s, f);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    if (e != hipSuccess) return e;
     const double G4 = 4.0 * sh.H;
     int nx = 0;
     for (int l = 0; l < L; ++l) nx += ly[l].Wt ? 1 : 0;
