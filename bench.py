@@ -26,8 +26,8 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
-PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix / vector peak
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 matrix peak (256 CUs x 4096 FLOP/clk x 2.4 GHz)
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 GEMM_CLASSES = ("gemm_input_proj", "gemm_dx", "gemm_dw", "gemm_dr", "gemm_dw_dr", "gemm_dp")
@@ -62,35 +62,72 @@ def workload_name(wl) -> str:
     return f"{base}_L{len(wl.layers)}_I{L0.I}_H{L0.H}{hp}_T{wl.T}_B{wl.B}"
 
 
-def cpu_baseline(wl, rows: int):
-    """The oracle, untuned, on the first `rows` batch rows of the same
-    workload (rows are independent, so the work per row is the full
-    problem's); reported in the same unit as `value`."""
-    import numpy as np
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_step_seconds(prob, sel):
+    """Wall time of one oracle forward + backward of the stack on batch rows `sel`."""
     import oracle
-    import synth
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     from _gpu_helpers import oracle_layers
-
-    prob = synth.draw(wl)
-    sel = np.arange(min(rows, wl.B))
     layers = oracle_layers(prob)
+    if len(sel) < prob.wl.B:
+        from _gpu_helpers import _rows_of
+        layers = [oracle.LayerDef([_rows_of(p, sel) for p in L.dirs], L.residual) for L in layers]
     x = prob.x.f64[:, sel]
     dy = prob.dy.f64[:, sel]
     t0 = time.perf_counter()
     oracle.stack_forward(x, layers)
     oracle.stack_backward(x, layers, dy)
-    dt = time.perf_counter() - t0
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(wl, rows: int):
+    """The oracle, untuned, on the first `rows` batch rows of the same
+    workload (rows are independent, so the work per row is the full
+    problem's) with every host core; reported in the same unit as `value`.
+    Also one thread on one row of the same workload and on the tiny
+    configuration (forward + backward, whole problem)."""
+    import numpy as np
+    import oracle
+    import synth
+
+    prob = synth.draw(wl)
+    sel = np.arange(min(rows, wl.B))
+    threads = oracle.num_threads()
+    dt = _oracle_step_seconds(prob, sel)
     frac = len(sel) / wl.B
     flops = wl.gemm_flops() * frac
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+    oracle.set_num_threads(1)
+    try:
+        dt1 = _oracle_step_seconds(prob, np.arange(1))
+        tiny = synth.tiny("f32")
+        dtt = min(_oracle_step_seconds(synth.draw(tiny), np.arange(tiny.B)) for _ in range(3))
+    finally:
+        oracle.set_num_threads(threads)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(sel)} of {wl.B} batch rows of the same stack (all layers, all {wl.T} steps), "
-                      f"forward + backward, fp64; {dt:.1f} s wall"}
+                      f"forward + backward, fp64; {dt:.1f} s wall",
+            "nproc": os.cpu_count(), "cpu_model": _cpu_model(),
+            "single_thread": {
+                "value": wl.gemm_flops() / wl.B / dt1 / 1e12, "unit": "TFLOP/s",
+                "sample": f"1 of {wl.B} batch rows of the same stack, 1 thread; {dt1:.1f} s wall",
+                "tiny_config_ms_per_step": dtt * 1e3,
+                "tiny_config": "1 layer, T=8, B=4, I=32, H=64, forward + backward, 1 thread"}}
 
 
-# Kernel classes whose launches are one kernel each, by kernel-name prefix
-# (for attributing the per-dispatch counter values to a class).
-CLASS_KERNELS = {"recurrent_fwd": "lstm_fwd_xcd", "recurrent_bwd": "lstm_bwd_xcd"}
+# Kernel classes whose launches are one kernel each, by kernel-name prefixes
+# (for attributing the per-dispatch counter values to a class): the XCD-local
+# recurrences, or the layer wavefront's at small batches.
+CLASS_KERNELS = {"recurrent_fwd": ("lstm_fwd_xcd", "lstm_fwd_wave"), "recurrent_bwd": ("lstm_bwd_xcd", "lstm_bwd_wave")}
 
 
 def _short_kernel(name: str) -> str:
@@ -134,8 +171,8 @@ def traffic_from(pmc_dir: str, workload: str, copy_mib: int):
         if k in write:
             by_name[k] = (fetch[k][1] * fetch_factor + write[k][1] * write_factor) * 1024.0
     kernels = {}
-    for cls, prefix in CLASS_KERNELS.items():
-        hits = [v for k, v in by_name.items() if k.startswith(prefix)]
+    for cls, prefixes in CLASS_KERNELS.items():
+        hits = [v for k, v in by_name.items() if k.startswith(prefixes)]
         if len(hits) == 1:
             kernels[cls] = {"hbm_bytes_per_launch": hits[0]}
     out = {"source_hash": kernel_source_hash(), "workload": workload, "fetch_factor": fetch_factor,
@@ -191,8 +228,7 @@ def main():
 
     import synth
     from paper_1907_13257_amd import Stack, lstm355
-    sys.path.insert(0, os.path.join(ROOT, "tests"))
-    from _gpu_helpers import device_params, stack_layers, to_dev
+    from synth.device import device_params, stack_layers, to_dev
 
     wl = make_workload(args)
     prob = synth.draw(wl)
@@ -214,13 +250,23 @@ def main():
     if st != 0:
         raise SystemExit(f"watchdog tripped during warmup ({lstm355.lstm_status_string(st)})")
 
-    # uninstrumented timing
+    # uninstrumented timing: wall clock over all steps, and one pair of HIP
+    # events per step on the stream the library runs on (median, min, p90)
+    cur = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for e0, e1 in evs:
+        e0.record(cur)
         step()
+        e1.record(cur)
     torch.cuda.synchronize()
     ms_plain = (time.perf_counter() - t0) * 1e3 / args.steps
+    per_step = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+
+    def pct(q):
+        return per_step[min(len(per_step) - 1, int(round(q * (len(per_step) - 1))))]
+    step_stats = {"median": pct(0.5), "min": per_step[0], "p90": pct(0.9), "max": per_step[-1]}
 
     # timed region with per-kernel events
     prof = not args.no_profile
@@ -268,11 +314,6 @@ def main():
             ent = tr.get("kernels", {}).get(dom)
             if ent and tr.get("source_hash") == kernel_source_hash() and tr.get("workload") == workload_name(wl):
                 traffic = ent.get("hbm_bytes_per_launch")
-        if dom in GEMM_CLASSES or dom.startswith("recurrent"):
-            # recurrent kernels run their dependent products on the matrix
-            # cores too, but are bound by the per-step barrier and traffic;
-            # they are reported against HBM with their algorithmic bytes.
-            pass
         if dom in GEMM_CLASSES:
             ach = s["flops"] / s["launches"] / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
@@ -281,6 +322,12 @@ def main():
             ach = s["bytes"] / s["launches"] / avg_s / 1e9
             roofline = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+            if dom.startswith("recurrent"):
+                # HBM is the only roofline that applies to the recurrences, but
+                # their counters (matrix cores and LDS a fraction busy, traffic
+                # far below peak) show the per-step wait between workgroups sets
+                # their time
+                roofline["limited_by"] = "per-step latency of the exchange between workgroups"
         gf = sum(stats[k]["flops"] for k in GEMM_CLASSES if k in stats)
         gt = sum(stats[k]["total_ms"] for k in GEMM_CLASSES if k in stats)
         if gt > 0:
@@ -299,6 +346,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_plain,
+        "ms_per_step_events": step_stats,
         "ms_per_step_with_kernel_events": ms,
         "higher_is_better": True,
         "scaling": "weak",

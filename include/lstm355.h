@@ -30,6 +30,10 @@
  *     validated on the host before anything is launched.
  *   - Calls on one handle that use the same workspace must be ordered (same
  *     stream); overlapping calls need distinct workspaces.
+ *   - `reserve_bytes` / `workspace_bytes` give the sizes of the caller's
+ *     reserve and workspace.  A call whose buffers are shorter than the sizes
+ *     its query functions report returns LSTM_ERR_WORKSPACE before anything
+ *     is launched (the device is not touched).
  */
 #ifndef LSTM355_H
 #define LSTM355_H
@@ -47,7 +51,7 @@ typedef enum {
     LSTM_OK = 0,
     LSTM_ERR_INVALID_ARG = 1,  /* bad size, NULL required pointer, misalignment */
     LSTM_ERR_UNSUPPORTED = 2,  /* shape has no kernel configuration on this device */
-    LSTM_ERR_WORKSPACE = 3,    /* reserved for size mismatches of caller buffers */
+    LSTM_ERR_WORKSPACE = 3,    /* a reserve or workspace shorter than the call needs */
     LSTM_ERR_HIP = 4,          /* a HIP runtime call or kernel launch failed */
     LSTM_ERR_TIMEOUT = 5       /* a grid barrier's watchdog expired (see lstm_check) */
 } lstm_status_t;
@@ -88,7 +92,8 @@ lstm_status_t lstm_forward(lstm_handle_t h,
                            const void *x, const void *h0, const float *c0,
                            const void *W, const void *R, const float *b, const void *P,
                            void *y, void *hT, float *cT,
-                           void *reserve, void *workspace, void *stream);
+                           void *reserve, size_t reserve_bytes,
+                           void *workspace, size_t workspace_bytes, void *stream);
 
 /* Forward pass of a stack of L unidirectional LSTM layers run as one layer
  * wavefront: layer l+1 starts a time step as soon as layer l has produced
@@ -104,7 +109,8 @@ lstm_status_t lstm_forward(lstm_handle_t h,
  *   W[l], R[l], b[l]: parameters of layer l.
  *   y[l]: output of layer l [T][B][H] (the input of layer l+1).
  *   reserve[l]: reserve of layer l (lstm_reserve_size(h[l]) bytes), for
- *     lstm_backward on h[l] exactly as after lstm_forward.
+ *     lstm_backward on h[l] exactly as after lstm_forward; reserve_bytes is
+ *     the size of each of them.
  *   workspace: at least the largest lstm_workspace_size of the handles.
  * Runs when L is 2..4, H = 1024 and B <= 32 on an MI355X whose XCD-local
  * path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the caller
@@ -112,7 +118,8 @@ lstm_status_t lstm_forward(lstm_handle_t h,
  * call may have written). */
 lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *h, const void *x,
                                  const void *const *W, const void *const *R, const float *const *b,
-                                 void *const *y, void *const *reserve, void *workspace, void *stream);
+                                 void *const *y, void *const *reserve, size_t reserve_bytes,
+                                 void *workspace, size_t workspace_bytes, void *stream);
 
 /* Back-propagation through time for the loss
  *   L = sum_t <dy_t, y_t> + <dhT, h_final> + <dcT, c_final>,
@@ -130,10 +137,10 @@ lstm_status_t lstm_backward(lstm_handle_t h,
                             const void *dy, const void *dhT, const float *dcT,
                             const void *x, const void *h0, const float *c0,
                             const void *W, const void *R, const void *P,
-                            const void *y, const void *reserve,
+                            const void *y, const void *reserve, size_t reserve_bytes,
                             void *dx, void *dh0, float *dc0,
                             float *dW, float *dR, float *db, float *dP,
-                            int accumulate, void *workspace, void *stream);
+                            int accumulate, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Backward pass of a stack run forward by lstm_forward_stack, as a layer
  * wavefront: layer l-1's BPTT step t starts as soon as layer l has produced
@@ -142,7 +149,7 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  * of one after another; the weight gradients follow per layer.  The result
  * equals lstm_backward on each layer from the top down, with dy of layer l-1
  * = dx of layer l, zero initial states and no gradient for the final states.
- *   h[l], W[l], R[l], y[l], reserve[l]: as given to lstm_forward_stack
+ *   h[l], W[l], R[l], y[l], reserve[l], reserve_bytes: as given to lstm_forward_stack
  *     (every layer with I = H: the stack's input x has the layers' width).
  *   dy: gradient of the top layer's output y[L-1], [T][B][H].
  *   x: the stack's input (layer 0's input).
@@ -150,14 +157,16 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  *   dW[l], dR[l], db[l]: fp32 weight gradients of layer l; accumulate as for
  *     lstm_backward.
  *   workspace: lstm_backward_stack_workspace_size(L, h) bytes (per-layer R^T,
- *     W^T and dz, and the gradients passed between layers).
+ *     W^T and dz, and the gradients passed between layers); workspace_bytes
+ *     is its size.
  * Runs when L is 2..4, T >= 2, H = 1024 and B <= 32 on an MI355X whose
  * XCD-local path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the
  * caller runs lstm_backward layer by layer. */
 lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *h, const void *dy, const void *x,
                                   const void *const *W, const void *const *R, const void *const *y,
-                                  const void *const *reserve, void *dx, float *const *dW, float *const *dR,
-                                  float *const *db, int accumulate, void *workspace, void *stream);
+                                  const void *const *reserve, size_t reserve_bytes, void *dx,
+                                  float *const *dW, float *const *dR, float *const *db, int accumulate,
+                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /* Workspace bytes lstm_backward_stack needs for these layers; 0 when the
  * stack's shapes do not fit the backward layer wavefront. */

@@ -54,12 +54,19 @@ def _load():
         lib.lstm_oracle_backward.restype = i
         lib.lstm_oracle_num_threads.argtypes = []
         lib.lstm_oracle_num_threads.restype = i
+        lib.lstm_oracle_set_num_threads.argtypes = [i]
+        lib.lstm_oracle_set_num_threads.restype = None
         _lib = lib
     return _lib
 
 
 def num_threads() -> int:
     return int(_load().lstm_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's loops (timing only; results do not depend on it)."""
+    _load().lstm_oracle_set_num_threads(int(n))
 
 
 def _in(a) -> Optional[np.ndarray]:

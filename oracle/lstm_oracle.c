@@ -58,6 +58,17 @@ int lstm_oracle_num_threads(void)
 #endif
 }
 
+/* Thread count of the loops below (timing only; the results do not depend
+ * on it: every output element is summed by one thread in a fixed order). */
+void lstm_oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Time index of the s-th visited step. */
 static long step_time(int s, int T, int reverse) { return reverse ? (long)(T - 1 - s) : (long)s; }
 

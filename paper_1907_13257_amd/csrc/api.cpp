@@ -58,6 +58,12 @@ lstm_status_t invalid(const char *what)
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+lstm_status_t short_buffer(const char *what, size_t given, size_t need)
+{
+    std::snprintf(g_detail, sizeof(g_detail), "%s: %zu bytes given, %zu needed", what, given, need);
+    return LSTM_ERR_WORKSPACE;
+}
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 lstm_status_t ensure_plan(lstm_handle *h)
@@ -191,7 +197,8 @@ extern "C" lstm_status_t lstm_destroy(lstm_handle_t h)
 
 extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
                                       const void *R, const float *b, const void *P, void *y, void *hT, float *cT,
-                                      void *reserve, void *workspace, void *stream)
+                                      void *reserve, size_t reserve_bytes, void *workspace, size_t workspace_bytes,
+                                      void *stream)
 {
     try {
         if (!h) return invalid("handle is NULL");
@@ -202,6 +209,8 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
             if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
         for (const void *p : {(const void *)c0, (const void *)b, (const void *)cT})
             if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+        if (reserve_bytes < h->r_total) return short_buffer("reserve", reserve_bytes, h->r_total);
+        if (workspace_bytes < h->w_total) return short_buffer("workspace", workspace_bytes, h->w_total);
         lstm_status_t st = ensure_plan(h);
         if (st != LSTM_OK) return st;
         hipStream_t s = static_cast<hipStream_t>(stream);
@@ -245,7 +254,8 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
 
 extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, const void *x, const void *const *W,
                                             const void *const *R, const float *const *b, void *const *y,
-                                            void *const *reserve, void *workspace, void *stream)
+                                            void *const *reserve, size_t reserve_bytes, void *workspace,
+                                            size_t workspace_bytes, void *stream)
 {
     try {
         if (L < 1 || !hs || !x || !W || !R || !b || !y || !reserve || !workspace)
@@ -257,6 +267,10 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
             if (!aligned4(b[l])) return invalid("fp32 tensors must be 4-byte aligned");
         }
         if (!aligned16(x) || !aligned16(workspace)) return invalid("device tensors must be 16-byte aligned");
+        for (int l = 0; l < L; ++l) {
+            if (reserve_bytes < hs[l]->r_total) return short_buffer("reserve", reserve_bytes, hs[l]->r_total);
+            if (workspace_bytes < hs[l]->w_total) return short_buffer("workspace", workspace_bytes, hs[l]->w_total);
+        }
         auto unsupported = [](const char *why) {
             std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: %s", why);
             return LSTM_ERR_UNSUPPORTED;
@@ -371,9 +385,9 @@ extern "C" size_t lstm_backward_stack_workspace_size(int L, const lstm_handle_t 
 
 extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, const void *dy, const void *x,
                                              const void *const *W, const void *const *R, const void *const *y,
-                                             const void *const *reserve, void *dx, float *const *dW,
-                                             float *const *dR, float *const *db, int accumulate, void *workspace,
-                                             void *stream)
+                                             const void *const *reserve, size_t reserve_bytes, void *dx,
+                                             float *const *dW, float *const *dR, float *const *db, int accumulate,
+                                             void *workspace, size_t workspace_bytes, void *stream)
 {
     try {
         if (L < 1 || !hs || !dy || !x || !W || !R || !y || !reserve || !dW || !dR || !db || !workspace)
@@ -392,6 +406,12 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
         if (const char *why = stack_bwd_unfit(L, hs)) {
             std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: %s", why);
             return LSTM_ERR_UNSUPPORTED;
+        }
+        for (int l = 0; l < L; ++l)
+            if (reserve_bytes < hs[l]->r_total) return short_buffer("reserve", reserve_bytes, hs[l]->r_total);
+        {
+            const size_t need = stack_bwd_layout(L, hs[0]->d).total;
+            if (workspace_bytes < need) return short_buffer("workspace", workspace_bytes, need);
         }
         const lstm_desc_t &d0 = hs[0]->d;
         const int T = d0.T, B = d0.B, H = d0.H;
@@ -473,9 +493,9 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
 
 extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const void *dhT, const float *dcT,
                                        const void *x, const void *h0, const float *c0, const void *W, const void *R,
-                                       const void *P, const void *y, const void *reserve, void *dx, void *dh0,
-                                       float *dc0, float *dW, float *dR, float *db, float *dP, int accumulate,
-                                       void *workspace, void *stream)
+                                       const void *P, const void *y, const void *reserve, size_t reserve_bytes,
+                                       void *dx, void *dh0, float *dc0, float *dW, float *dR, float *db, float *dP,
+                                       int accumulate, void *workspace, size_t workspace_bytes, void *stream)
 {
     try {
         if (!h) return invalid("handle is NULL");
@@ -490,6 +510,8 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         for (const void *p : {(const void *)dcT, (const void *)c0, (const void *)dc0, (const void *)dW,
                               (const void *)dR, (const void *)db, (const void *)dP})
             if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+        if (reserve_bytes < h->r_total) return short_buffer("reserve", reserve_bytes, h->r_total);
+        if (workspace_bytes < h->w_total) return short_buffer("workspace", workspace_bytes, h->w_total);
         lstm_status_t st = ensure_plan(h);
         if (st != LSTM_OK) return st;
         hipStream_t s = static_cast<hipStream_t>(stream);

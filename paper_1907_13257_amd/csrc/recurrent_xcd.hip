@@ -1078,6 +1078,29 @@ bool wave_path_ok(const RecShape &sh, int num_cus)
            sh.B >= 1 && sh.B <= 32 && sh.ldy == sh.H && (long)sh.T * sh.B * 4L * sh.H * 4 <= 0x7fffffffL;
 }
 
+namespace {
+// Rows the forward layer wavefront exchanges, armed before its launch: y of
+// each layer (dense, two NOT_READY halves per word) and the input projections
+// that the projection XCDs write; the flags start at zero.
+FillRanges forward_wave_fills(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync)
+{
+    const long rows = (long)sh.T * sh.B;
+    FillRanges f{};
+    int nr = 0;
+    f.p[nr] = sync + XCD_FLAGS; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
+    for (int l = 0; l < L && l < 4; ++l) {
+        f.p[nr] = static_cast<uint32_t *>(ly[l].y); f.n[nr] = rows * sh.H / 2;
+        f.v[nr++] = ((uint32_t)NOT_READY << 16) | NOT_READY;
+        if (l > 0 || x) {
+            f.p[nr] = reinterpret_cast<uint32_t *>(ly[l].gates); f.n[nr] = rows * 4 * sh.H;
+            f.v[nr++] = NOT_READY_F32;
+        }
+    }
+    f.count = nr;
+    return f;
+}
+}  // namespace
+
 hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
                                unsigned long long timeout, hipStream_t s)
 {
@@ -1095,27 +1118,13 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
     }
     a.flags = sync + XCD_FLAGS;
     a.timeout = timeout;
-    // every exchanged row waits for its producer: y of each layer (dense, two
-    // NOT_READY halves per word), and the input projections that the
-    // projection XCDs write; the flags start at zero
-    const long rows = (long)sh.T * sh.B;
-    FillRanges f{};
-    int nr = 0;
-    f.p[nr] = a.flags; f.n[nr] = XCD_WORDS; f.v[nr++] = 0u;
-    for (int l = 0; l < L; ++l) {
-        f.p[nr] = static_cast<uint32_t *>(ly[l].y); f.n[nr] = rows * sh.H / 2;
-        f.v[nr++] = ((uint32_t)NOT_READY << 16) | NOT_READY;
-        if (l > 0 || x) {
-            f.p[nr] = reinterpret_cast<uint32_t *>(ly[l].gates); f.n[nr] = rows * 4 * sh.H;
-            f.v[nr++] = NOT_READY_F32;
-        }
-    }
+    const FillRanges f = forward_wave_fills(sh, L, x, ly, sync);
     hipError_t e;
     {
         double bytes = 0.0;
-        for (int r = 0; r < nr; ++r) bytes += 4.0 * f.n[r];
+        for (int r = 0; r < f.count; ++r) bytes += 4.0 * f.n[r];
         ProfScope pf(K_SMALL, s, 0.0, bytes);
-        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, nr), dim3(256), 0, s, f);
+        hipLaunchKernelGGL(fill_ranges_kernel, dim3(256, f.count), dim3(256), 0, s, f);
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

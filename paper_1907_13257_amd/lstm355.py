@@ -55,10 +55,10 @@ def load_library():
         "lstm_create": ([ctypes.POINTER(lstm_desc_t), ctypes.POINTER(H)], i),
         "lstm_reserve_size": ([H], sz),
         "lstm_workspace_size": ([H], sz),
-        "lstm_forward": ([H] + [vp] * 13, i),
-        "lstm_backward": ([H] + [vp] * 18 + [i, vp, vp], i),
-        "lstm_forward_stack": ([i] + [vp] * 9, i),
-        "lstm_backward_stack": ([i] + [vp] * 11 + [i, vp, vp], i),
+        "lstm_forward": ([H] + [vp] * 11 + [sz, vp, sz, vp], i),
+        "lstm_backward": ([H] + [vp] * 11 + [sz] + [vp] * 7 + [i, vp, sz, vp], i),
+        "lstm_forward_stack": ([i] + [vp] * 7 + [sz, vp, sz, vp], i),
+        "lstm_backward_stack": ([i] + [vp] * 7 + [sz] + [vp] * 4 + [i, vp, sz, vp], i),
         "lstm_backward_stack_workspace_size": ([i, vp], sz),
         "lstm_check": ([H, vp, vp], i),
         "lstm_destroy": ([H], i),
@@ -100,6 +100,15 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _nbytes(t, given=None) -> int:
+    """Size of a buffer: `given` when stated, else a torch tensor's bytes."""
+    if given is not None:
+        return int(given)
+    if t is None or isinstance(t, int):
+        raise ValueError("the size of a raw-pointer buffer must be given")
+    return t.numel() * t.element_size()
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -128,9 +137,11 @@ def lstm_workspace_size(h) -> int:
     return load_library().lstm_workspace_size(h)
 
 
-def lstm_forward(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, workspace, stream=None):
+def lstm_forward(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, workspace, stream=None, reserve_bytes=None,
+                 workspace_bytes=None):
     _check(load_library().lstm_forward(h, _ptr(x), _ptr(h0), _ptr(c0), _ptr(W), _ptr(R), _ptr(b), _ptr(P), _ptr(y),
-                                       _ptr(hT), _ptr(cT), _ptr(reserve), _ptr(workspace), _stream(stream)),
+                                       _ptr(hT), _ptr(cT), _ptr(reserve), _nbytes(reserve, reserve_bytes),
+                                       _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream)),
            "lstm_forward")
 
 
@@ -141,7 +152,8 @@ def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=N
     n = len(handles)
     arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
     st = load_library().lstm_forward_stack(n, arr(handles), _ptr(x), arr(Ws), arr(Rs), arr(bs), arr(ys),
-                                           arr(reserves), _ptr(workspace), _stream(stream))
+                                           arr(reserves), min(_nbytes(r) for r in reserves), _ptr(workspace),
+                                           _nbytes(workspace), _stream(stream))
     if st == LSTM_ERR_UNSUPPORTED:
         return False
     _check(st, "lstm_forward_stack")
@@ -161,8 +173,9 @@ def lstm_backward_stack(handles, dy, x, Ws, Rs, ys, reserves, dx, dWs, dRs, dbs,
     n = len(handles)
     arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
     st = load_library().lstm_backward_stack(n, arr(handles), _ptr(dy), _ptr(x), arr(Ws), arr(Rs), arr(ys),
-                                            arr(reserves), _ptr(dx), arr(dWs), arr(dRs), arr(dbs),
-                                            int(bool(accumulate)), _ptr(workspace), _stream(stream))
+                                            arr(reserves), min(_nbytes(r) for r in reserves), _ptr(dx), arr(dWs),
+                                            arr(dRs), arr(dbs), int(bool(accumulate)), _ptr(workspace),
+                                            _nbytes(workspace), _stream(stream))
     if st == LSTM_ERR_UNSUPPORTED:
         return False
     _check(st, "lstm_backward_stack")
@@ -170,11 +183,12 @@ def lstm_backward_stack(handles, dy, x, Ws, Rs, ys, reserves, dx, dWs, dRs, dbs,
 
 
 def lstm_backward(h, dy, dhT, dcT, x, h0, c0, W, R, P, y, reserve, dx, dh0, dc0, dW, dR, db, dP, accumulate,
-                  workspace, stream=None):
+                  workspace, stream=None, reserve_bytes=None, workspace_bytes=None):
     _check(load_library().lstm_backward(h, _ptr(dy), _ptr(dhT), _ptr(dcT), _ptr(x), _ptr(h0), _ptr(c0), _ptr(W),
-                                        _ptr(R), _ptr(P), _ptr(y), _ptr(reserve), _ptr(dx), _ptr(dh0), _ptr(dc0),
-                                        _ptr(dW), _ptr(dR), _ptr(db), _ptr(dP), int(bool(accumulate)),
-                                        _ptr(workspace), _stream(stream)),
+                                        _ptr(R), _ptr(P), _ptr(y), _ptr(reserve), _nbytes(reserve, reserve_bytes),
+                                        _ptr(dx), _ptr(dh0), _ptr(dc0), _ptr(dW), _ptr(dR), _ptr(db), _ptr(dP),
+                                        int(bool(accumulate)), _ptr(workspace), _nbytes(workspace, workspace_bytes),
+                                        _stream(stream)),
            "lstm_backward")
 
 

@@ -245,12 +245,21 @@ def draw(wl: Workload, row_mask: Optional[np.ndarray] = None) -> Problem:
     return Problem(wl, params, x, h0, c0, dy)
 
 
-def sample_rows(B: int, n: int, seed: int) -> np.ndarray:
-    """A seeded choice of `n` distinct batch rows (always including the first
-    and the last row, so ragged tails are covered)."""
-    rng = np.random.Generator(np.random.PCG64(10_000 + seed))
-    n = min(n, B)
+def sample_rows_blocks(B: int, seed: int, parts: int = 8, block: int = 16) -> np.ndarray:
+    """A seeded sample of batch rows that touches every (part, row block)
+    pair of a batch split into `parts` contiguous shares of ceil(B/parts)
+    rows, each cut into blocks of `block` rows: per block one random row,
+    plus its first row (even blocks) or its last row (odd blocks); the
+    batch's first and last rows are always included."""
+    rng = np.random.Generator(np.random.PCG64(20_000 + seed))
+    share = (B + parts - 1) // parts
     rows = {0, B - 1}
-    while len(rows) < n:
-        rows.add(int(rng.integers(0, B)))
-    return np.array(sorted(rows)[:n], dtype=np.int64)
+    k = 0
+    for p in range(parts):
+        lo, hi = p * share, min(B, p * share + share)
+        for b0 in range(lo, hi, block):
+            b1 = min(hi, b0 + block)
+            rows.add(int(rng.integers(b0, b1)))
+            rows.add(b0 if k % 2 == 0 else b1 - 1)
+            k += 1
+    return np.array(sorted(rows), dtype=np.int64)

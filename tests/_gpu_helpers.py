@@ -10,6 +10,7 @@ import numpy as np
 
 import oracle
 import synth
+from synth.device import device_params, stack_layers, to_dev, to_f64  # noqa: F401
 
 TOL = {"f32": dict(out=1e-4, grad=1e-4), "bf16": dict(out=2e-2, grad=5e-2)}
 
@@ -26,25 +27,6 @@ def normwise(a, r) -> float:
 def announce(msg: str):
     print(f"[gpu-case] {msg}", flush=True)
     sys.stdout.flush()
-
-
-def to_dev(t, device="cuda"):
-    import torch
-    if t is None:
-        return None
-    if isinstance(t, synth.Tensor):
-        if t.dtype == "bf16":
-            return torch.from_numpy(t.dev.view(np.int16)).view(torch.bfloat16).to(device)
-        return torch.from_numpy(t.dev).to(device)
-    return torch.from_numpy(np.ascontiguousarray(t)).to(device)
-
-
-def to_f64(x) -> np.ndarray:
-    import torch
-    x = x.detach()
-    if x.dtype == torch.bfloat16:
-        return synth.bf16_bits_to_f64(x.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
-    return x.double().cpu().numpy()
 
 
 def oracle_layers(prob: synth.Problem) -> List[oracle.LayerDef]:
@@ -88,24 +70,6 @@ def run_oracle(prob: synth.Problem, rows: Optional[np.ndarray] = None) -> Dict:
     y, _ = oracle.stack_forward(x, layers)
     g = oracle.stack_backward(x, layers, dy)
     return dict(y=y, dx=g["dx"], layers=g["layers"])
-
-
-def stack_layers(wl: synth.Workload):
-    from paper_1907_13257_amd import StackLayer
-    return [StackLayer(L.I, L.H, L.Hp, L.bidirectional, L.residual) for L in wl.layers]
-
-
-def device_params(prob: synth.Problem):
-    params = []
-    for li, L in enumerate(prob.wl.layers):
-        dl = []
-        for p in prob.params[li]:
-            d = dict(W=to_dev(p.W), R=to_dev(p.R), b=to_dev(p.b))
-            if p.P is not None:
-                d["P"] = to_dev(p.P)
-            dl.append(d)
-        params.append(dl)
-    return params
 
 
 def run_stack_gpu(prob: synth.Problem, stack=None, params=None):

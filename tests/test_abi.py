@@ -66,23 +66,58 @@ def test_sizes_and_destroy(lib):
 def test_forward_backward_validate_before_launch(lib):
     h = L.lstm_create(4, 3, 32, 16, 0, "bf16")
     A = 1 << 20  # a 16-byte aligned stand-in address; validation fails before any use
+    R, WS = L.lstm_reserve_size(h), L.lstm_workspace_size(h)
+
+    def fwd(hh, x=A, P=None, rb=R, wb=WS):
+        return lib.lstm_forward(hh, x, None, None, A, A, A, P, A, None, None, A, rb, A, wb, None)
+
     # missing required pointers
-    assert lib.lstm_forward(h, None, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert fwd(h, x=None) == L.LSTM_ERR_INVALID_ARG
     # P given to a plain LSTM
-    assert lib.lstm_forward(h, A, None, None, A, A, A, A, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert fwd(h, P=A) == L.LSTM_ERR_INVALID_ARG
     # misaligned activation pointer
-    assert lib.lstm_forward(h, A + 2, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    assert fwd(h, x=A + 2) == L.LSTM_ERR_INVALID_ARG
     assert "aligned" in L.lstm_last_error_detail()
+    assert fwd(None) == L.LSTM_ERR_INVALID_ARG
+
     # backward: missing weight gradients, bad accumulate flag
-    args = [A, None, None, A, None, None, A, A, None, A, A, None, None, None, A, A, A, None]
-    assert lib.lstm_backward(h, *args[:14], None, A, A, None, 0, A, None) == L.LSTM_ERR_INVALID_ARG
-    assert lib.lstm_backward(h, *args, 2, A, None) == L.LSTM_ERR_INVALID_ARG
-    assert lib.lstm_forward(None, A, None, None, A, A, A, None, A, None, None, A, A, None) == L.LSTM_ERR_INVALID_ARG
+    def bwd(hh, P=None, dW=A, dP=None, acc=0, rb=R, wb=WS):
+        return lib.lstm_backward(hh, A, None, None, A, None, None, A, A, P, A, A, rb, None, None, None,
+                                 dW, A, A, dP, acc, A, wb, None)
+
+    assert bwd(h, dW=None) == L.LSTM_ERR_INVALID_ARG
+    assert bwd(h, acc=2) == L.LSTM_ERR_INVALID_ARG
     hp = L.lstm_create(4, 3, 32, 16, 8, "bf16")
-    args_p = [A, None, None, A, None, None, A, A, A, A, A, None, None, None, A, A, A, None]
-    assert lib.lstm_backward(hp, *args_p, 0, A, None) == L.LSTM_ERR_INVALID_ARG   # dP missing
+    Rp, WSp = L.lstm_reserve_size(hp), L.lstm_workspace_size(hp)
+    assert bwd(hp, P=A, rb=Rp, wb=WSp) == L.LSTM_ERR_INVALID_ARG   # dP missing
     L.lstm_destroy(h)
     L.lstm_destroy(hp)
+
+
+def test_short_buffers_are_rejected_before_launch(lib):
+    """A reserve or workspace shorter than the query functions report is
+    LSTM_ERR_WORKSPACE, decided on the host (no device is touched)."""
+    A = 1 << 20
+    for Hp in (0, 8):
+        h = L.lstm_create(5, 3, 32, 16, Hp, "bf16")
+        R, WS = L.lstm_reserve_size(h), L.lstm_workspace_size(h)
+        P = A if Hp else None
+        dP = A if Hp else None
+
+        def fwd(rb, wb):
+            return lib.lstm_forward(h, A, None, None, A, A, A, P, A, None, None, A, rb, A, wb, None)
+
+        def bwd(rb, wb):
+            return lib.lstm_backward(h, A, None, None, A, None, None, A, A, P, A, A, rb, None, None, None,
+                                     A, A, A, dP, 0, A, wb, None)
+
+        for call in (fwd, bwd):
+            assert call(R - 1, WS) == L.LSTM_ERR_WORKSPACE
+            assert "reserve" in L.lstm_last_error_detail() and str(R) in L.lstm_last_error_detail()
+            assert call(R, WS - 256) == L.LSTM_ERR_WORKSPACE
+            assert "workspace" in L.lstm_last_error_detail()
+            assert call(0, 0) == L.LSTM_ERR_WORKSPACE
+        L.lstm_destroy(h)
 
 
 def test_forward_stack_validates_before_launch(lib):
@@ -95,14 +130,19 @@ def test_forward_stack_validates_before_launch(lib):
     arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
     ptrs = lambda n: arr([A] * n)
 
-    def call(hs, x=A, n=None):
+    BIG = 1 << 60
+
+    def call(hs, x=A, n=None, rb=BIG, wb=BIG):
         n = len(hs) if n is None else n
-        return lib.lstm_forward_stack(n, arr(hs), x, ptrs(n), ptrs(n), ptrs(n), ptrs(n), ptrs(n), A, None)
+        return lib.lstm_forward_stack(n, arr(hs), x, ptrs(n), ptrs(n), ptrs(n), ptrs(n), ptrs(n), rb, A, wb, None)
 
     assert call(hb[:2], x=None) == L.LSTM_ERR_INVALID_ARG                  # missing input
     assert call(hb[:2], x=A + 2) == L.LSTM_ERR_INVALID_ARG                 # misaligned input
     assert call(hb[:2], n=0) == L.LSTM_ERR_INVALID_ARG
     assert call([hb[0], None]) == L.LSTM_ERR_INVALID_ARG                  # missing handle
+    need_r, need_w = L.lstm_reserve_size(hb[0]), L.lstm_workspace_size(hb[0])
+    assert call(hb[:2], rb=need_r - 1) == L.LSTM_ERR_WORKSPACE             # short reserves
+    assert call(hb[:2], wb=need_w - 1) == L.LSTM_ERR_WORKSPACE             # short workspace
     assert call(hb[:1]) == L.LSTM_ERR_UNSUPPORTED                          # one layer
     assert call(hb[:5]) == L.LSTM_ERR_UNSUPPORTED                          # five layers
     assert call(hf) == L.LSTM_ERR_UNSUPPORTED                              # fp32
@@ -129,16 +169,21 @@ def test_backward_stack_validates_before_launch(lib):
     hn = L.lstm_create(6, 8, 512, 1024, 0, "bf16")
     assert L.lstm_backward_stack_workspace_size([hn, hb[0]]) == 0      # layer 0 input narrower than H
 
-    def call(hs, dy=A, acc=0):
+    BIG = 1 << 60
+
+    def call(hs, dy=A, acc=0, rb=BIG, wb=BIG):
         n = len(hs)
         p = arr([A] * n)
-        return lib.lstm_backward_stack(n, arr(hs), dy, A, p, p, p, p, None, p, p, p, acc, A, None)
+        return lib.lstm_backward_stack(n, arr(hs), dy, A, p, p, p, p, rb, None, p, p, p, acc, A, wb, None)
 
     assert call(hb, dy=None) == L.LSTM_ERR_INVALID_ARG
     assert call(hb, acc=2) == L.LSTM_ERR_INVALID_ARG
     assert call(hb, dy=A + 2) == L.LSTM_ERR_INVALID_ARG
     assert call([hn, hb[0]]) == L.LSTM_ERR_UNSUPPORTED
     assert call([h1, h1]) == L.LSTM_ERR_UNSUPPORTED
+    assert call(hb, rb=L.lstm_reserve_size(hb[0]) - 1) == L.LSTM_ERR_WORKSPACE
+    assert call(hb, wb=size - 1) == L.LSTM_ERR_WORKSPACE
+    assert "workspace" in L.lstm_last_error_detail()
     for h in hb + [h1, hn]:
         L.lstm_destroy(h)
 

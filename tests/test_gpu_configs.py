@@ -2,8 +2,11 @@
 benchmark times.
 
 The oracle cannot run a whole full-size step in test time, so the GPU runs
-the full mini-batch with the upstream gradient kept only on a few sampled
-batch rows (zero elsewhere).  Batch rows are independent in the LSTM, so
+the full mini-batch with the upstream gradient kept only on sampled batch
+rows (zero elsewhere).  The sample touches every (XCD, 16-row block) pair of
+the XCD-local recurrences (XCD x owns rows [x*RX, x*RX + RX), RX =
+ceil(B/8), in blocks of 16), with the first or last row of each block, so
+every row-block code path and every XCD's share is compared.  Batch rows are independent in the LSTM, so
   - outputs and input gradients of the sampled rows equal the oracle's on
     those rows alone, and
   - every weight gradient equals the oracle's weight gradient over the
@@ -26,8 +29,8 @@ def need_gpu():
         pytest.skip("no GPU")
 
 
-def run_masked(wl: synth.Workload, nrows=3):
-    rows = synth.sample_rows(wl.B, nrows, wl.seed)
+def run_masked(wl: synth.Workload):
+    rows = synth.sample_rows_blocks(wl.B, wl.seed)
     mask = np.zeros(wl.B, dtype=bool)
     mask[rows] = True
     announce(f"{wl.name} T{wl.T} B{wl.B} layers={len(wl.layers)} rows={rows.tolist()}")

@@ -125,6 +125,8 @@ LAYER_CASES = [
     (1, 9, 16, 256, 0, "bf16", True),      # a single step
     (3, 3, 32, 256, 0, "bf16", False),     # fewer rows than XCDs: five XCDs own no row
     (2, 1, 8, 1024, 0, "bf16", True),      # one row in all, full-width cells
+    (3, 136, 64, 1024, 0, "bf16", False),  # full-width cells, 17 rows per XCD: two row blocks
+    (3, 264, 64, 1024, 0, "bf16", True),   # full-width cells, 33 rows per XCD: four row blocks, reverse
     # [dW | dR] as one product (bf16, B a multiple of 32, I and I + H multiples of 128)
     (4, 32, 128, 256, 0, "bf16", False),   # with h0: the first step's segment comes from h0
     (3, 64, 128, 256, 0, "bf16", True),    # reverse: h0 pairs with the last time index
@@ -222,6 +224,39 @@ def test_zero_weights_closed_form(dtype, H):
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:
         xcd = dtype == "bf16"
         assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
+
+
+@pytest.mark.parametrize("T,B,I,H,dtype,must_trip", [(20, 24, 32, 72, "f32", True),
+                                                      (20, 64, 32, 256, "bf16", False)])
+def test_watchdog_gives_up_from_host_and_next_call_succeeds(T, B, I, H, dtype, must_trip, monkeypatch):
+    """A watchdog of 0 us, set from the host (LSTM355_WATCHDOG_US), makes the
+    persistent recurrence's waits give up instead of waiting: every wave
+    exits (the launch completes), lstm_check reports LSTM_ERR_TIMEOUT, and
+    the next calls with the normal watchdog give the oracle's results.  The
+    generic kernel's grid barrier always trips (the first workgroup to arrive
+    finds the others missing); the XCD-local kernel trips when any wave's
+    first copy of the exchanged rows is incomplete, which is not certain."""
+    from paper_1907_13257_amd import Layer, lstm355
+    label = f"watchdog T{T} B{B} I{I} H{H} {dtype}"
+    announce(label)
+    c = layer_case(T, B, I, H, 0, dtype, False, seed=T * 10 + B)
+    lay = Layer(T, B, I, H, 0, dtype, False)
+    d = {k: to_dev(v) for k, v in c.items()}
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = torch.empty((T, B, H), dtype=td, device="cuda")
+    monkeypatch.setenv("LSTM355_WATCHDOG_US", "0")
+    lay.forward(d["x"], d["W"], d["R"], d["b"], None, d["h0"], d["c0"], y)
+    st = lay.check()
+    monkeypatch.delenv("LSTM355_WATCHDOG_US")
+    announce(f"{label}: status after the forced watchdog {lstm355.lstm_status_string(st)}")
+    if must_trip:
+        assert st == lstm355.LSTM_ERR_TIMEOUT
+    else:
+        assert st in (lstm355.LSTM_OK, lstm355.LSTM_ERR_TIMEOUT)
+    assert lay.check() == lstm355.LSTM_OK   # the flag was cleared by the check
+    lay.close()
+    gpu = run_layer_gpu(c, T, B, I, H, 0, dtype, False)
+    check_layer(gpu, oracle_layer(c, 0, False), dtype, label + " after the trip")
 
 
 def test_layer_without_initial_state_or_final_grads():

@@ -464,3 +464,55 @@ def test_golden_regression():
         res = dict(o, **g)
         for k, v in case["expected"].items():
             assert normwise(res[k], np.array(v)) <= 1e-14, (case["name"], k)
+
+
+def test_torch_stack_cross_check():
+    """Stack composition against torch in float64 on the CPU, run as a black
+    box: torch.nn.LSTM(num_layers=2, bidirectional=True) for a bidirectional
+    first layer whose concatenated output feeds a bidirectional second layer,
+    then a unidirectional third layer with its residual added by hand.  The
+    oracle composes the same three layers with stack_forward / stack_backward
+    (concatenation order, split of the upstream gradient between directions,
+    summed input gradients, identity path of the residual)."""
+    rng = np.random.default_rng(31)
+    T, B, I, H = 5, 3, 6, 4
+    W = lambda *s: rng.uniform(-0.6, 0.6, s)
+    p = [[dict(W=W(4 * H, I), R=W(4 * H, H), b=W(4 * H)) for _ in range(2)],
+         [dict(W=W(4 * H, 2 * H), R=W(4 * H, H), b=W(4 * H)) for _ in range(2)],
+         [dict(W=W(4 * (2 * H), 2 * H), R=W(4 * (2 * H), 2 * H), b=W(4 * (2 * H)))]]
+    # the third layer has 2H cells so that its residual (output = y + input) is defined
+    x = rng.uniform(-1, 1, (T, B, I))
+    dy = rng.standard_normal((T, B, 2 * H))
+
+    m = torch.nn.LSTM(I, H, num_layers=2, bidirectional=True, dtype=torch.float64)
+    m3 = torch.nn.LSTM(2 * H, 2 * H, dtype=torch.float64)
+    with torch.no_grad():
+        for l in range(2):
+            for d, sfx in enumerate(("", "_reverse")):
+                getattr(m, f"weight_ih_l{l}{sfx}").copy_(torch.from_numpy(p[l][d]["W"]))
+                getattr(m, f"weight_hh_l{l}{sfx}").copy_(torch.from_numpy(p[l][d]["R"]))
+                getattr(m, f"bias_ih_l{l}{sfx}").copy_(torch.from_numpy(p[l][d]["b"]))
+                getattr(m, f"bias_hh_l{l}{sfx}").zero_()
+        m3.weight_ih_l0.copy_(torch.from_numpy(p[2][0]["W"]))
+        m3.weight_hh_l0.copy_(torch.from_numpy(p[2][0]["R"]))
+        m3.bias_ih_l0.copy_(torch.from_numpy(p[2][0]["b"]))
+        m3.bias_hh_l0.zero_()
+    xt = torch.from_numpy(x).requires_grad_(True)
+    y2, _ = m(xt)
+    y3, _ = m3(y2)
+    out = y3 + y2
+    (out * torch.from_numpy(dy)).sum().backward()
+
+    layers = [oracle.LayerDef(p[0]), oracle.LayerDef(p[1]), oracle.LayerDef(p[2], residual=True)]
+    o, _ = oracle.stack_forward(x, layers)
+    g = oracle.stack_backward(x, layers, dy)
+    assert normwise(o, out.detach().numpy()) <= 1e-12
+    assert normwise(g["dx"], xt.grad.numpy()) <= 1e-12
+    for l in range(2):
+        for d, sfx in enumerate(("", "_reverse")):
+            assert normwise(g["layers"][l][d]["dW"], getattr(m, f"weight_ih_l{l}{sfx}").grad.numpy()) <= 1e-12
+            assert normwise(g["layers"][l][d]["dR"], getattr(m, f"weight_hh_l{l}{sfx}").grad.numpy()) <= 1e-12
+            assert normwise(g["layers"][l][d]["db"], getattr(m, f"bias_ih_l{l}{sfx}").grad.numpy()) <= 1e-12
+    assert normwise(g["layers"][2][0]["dW"], m3.weight_ih_l0.grad.numpy()) <= 1e-12
+    assert normwise(g["layers"][2][0]["dR"], m3.weight_hh_l0.grad.numpy()) <= 1e-12
+    assert normwise(g["layers"][2][0]["db"], m3.bias_ih_l0.grad.numpy()) <= 1e-12

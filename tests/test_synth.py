@@ -53,3 +53,16 @@ def test_draw_is_reproducible_and_masked():
 def test_flop_count_headline():
     # 4 layers x 3 x 2*T*B*4H*(I+H) with T=50, B=128, I=H=1024
     assert abs(synth.gnmt4().gemm_flops() - 1288.49e9) < 0.01e9
+
+
+def test_block_sample_covers_every_share_and_block():
+    for B in (1, 3, 16, 20, 32, 64, 128, 256, 264, 512):
+        rows = synth.sample_rows_blocks(B, seed=B)
+        assert rows[0] == 0 and rows[-1] == B - 1 and len(set(rows.tolist())) == len(rows)
+        share = (B + 7) // 8
+        for p in range(8):
+            for b0 in range(p * share, min(B, p * share + share), 16):
+                b1 = min(B, p * share + share, b0 + 16)
+                assert np.any((rows >= b0) & (rows < b1)), (B, p, b0)
+    # 32 (share, block) pairs at B = 512, up to two rows each
+    assert 48 <= len(synth.sample_rows_blocks(512, seed=2)) <= 66
