@@ -95,6 +95,24 @@ lstm_status_t lstm_forward(lstm_handle_t h,
                            void *reserve, size_t reserve_bytes,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* lstm_forward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It calls no allocating routine: its
+ * scratch (the sync words of the persistent recurrences: barrier counter,
+ * abort word, per-XCD claim masks) lives in a 64 KiB array that the library
+ * keeps on each GPU until the process ends.  Arguments and results are those
+ * of lstm_forward.  Layers whose forward needs more scratch than that (the
+ * stepwise recurrence of wide LSTMP layers, whose split products need
+ * partial sums) return LSTM_ERR_WORKSPACE with the sizes in
+ * lstm_last_error_detail.  Every call on one GPU shares its array, so calls
+ * that overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller; each call clears what must start at zero. */
+lstm_status_t lstm_forward_noalloc(lstm_handle_t h,
+                                   const void *x, const void *h0, const float *c0,
+                                   const void *W, const void *R, const float *b, const void *P,
+                                   void *y, void *hT, float *cT,
+                                   void *reserve, size_t reserve_bytes, void *stream);
+
 /* Forward pass of a stack of L unidirectional LSTM layers run as one layer
  * wavefront: layer l+1 starts a time step as soon as layer l has produced
  * that step, so the layers advance together a few steps apart instead of one
@@ -184,7 +202,8 @@ size_t lstm_backward_stack_workspace_size(int L, const lstm_handle_t *h);
 /* Synchronises `stream` and reports whether any kernel of the library gave up
  * at a grid barrier on the current device since the last check
  * (LSTM_ERR_TIMEOUT; the device-wide flag is then cleared).  Outputs of such a
- * call are undefined.  `workspace` is the one the checked calls used. */
+ * call are undefined.  `workspace` (the one the checked calls used) may be
+ * NULL, as after lstm_forward_noalloc: the flags are kept per device. */
 lstm_status_t lstm_check(lstm_handle_t h, void *workspace, void *stream);
 
 /* Frees the handle.  NULL is a no-op. */

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "../../include/lstm355.h"
@@ -195,58 +196,144 @@ extern "C" lstm_status_t lstm_destroy(lstm_handle_t h)
     return LSTM_OK;
 }
 
+namespace {
+// Validation shared by the forward entry points (everything but the workspace).
+lstm_status_t check_forward_args(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
+                                 const void *R, const float *b, const void *P, const void *y, const void *hT,
+                                 const float *cT, const void *reserve, size_t reserve_bytes)
+{
+    if (!h) return invalid("handle is NULL");
+    const lstm_desc_t &d = h->d;
+    if (!x || !W || !R || !b || !y || !reserve) return invalid("required pointer is NULL");
+    if ((P != nullptr) != (d.Hp > 0)) return invalid("P must be given iff Hp > 0");
+    for (const void *p : {x, h0, W, R, P, y, hT, reserve})
+        if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+    for (const void *p : {(const void *)c0, (const void *)b, (const void *)cT})
+        if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
+    if (reserve_bytes < h->r_total) return short_buffer("reserve", reserve_bytes, h->r_total);
+    return LSTM_OK;
+}
+
+// One layer's forward pass (arguments validated, plan made): the input
+// projection, then the recurrence.  `wv` is the workspace (sync words at
+// w_sync; the stepwise recurrence also uses the split-K partials at w_split).
+lstm_status_t forward_impl(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
+                           const void *R, const float *b, const void *P, void *y, void *hT, float *cT,
+                           void *reserve, char *wv, hipStream_t s)
+{
+    const lstm_desc_t &d = h->d;
+    char *rv = static_cast<char *>(reserve);
+    float *gates = reinterpret_cast<float *>(rv + h->r_gates);
+
+    RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, h->ldy};
+    FwdBufs fb{};
+    fb.R = R; fb.P = P; fb.h0 = h0; fb.c0 = c0;
+    fb.gates = gates;
+    fb.cs = reinterpret_cast<float *>(rv + h->r_cs);
+    fb.ms = d.Hp ? rv + h->r_ms : nullptr;
+    fb.y = y; fb.hT = hT; fb.cT = cT;
+    fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
+    const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+
+    GemmDesc g{};
+    g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
+    g.M = (int)h->TB; g.N = (int)h->G4; g.K = d.I;
+    g.A = x; g.lda = h->ldx;
+    g.B = W; g.ldb = d.I;
+    g.C = gates; g.ldc = h->G4;
+    g.bias = b; g.beta = 0;
+    if (xcd) g.side = xcd_prep_forward(sh, fb);   // the recurrence's exchange rows and flags
+    TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
+
+    if (!xcd && use_stepwise(h, h->fwd_ok)) {
+        StepwiseArgs sw{R, P, reinterpret_cast<float *>(wv + h->w_split), h->split_floats};
+        TRY_HIP("forward recurrence (stepwise)", forward_stepwise(h->dt, sh, fb, sw, s));
+    } else if (xcd) {
+        TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s, true));
+    } else {
+        TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
+    }
+    return LSTM_OK;
+}
+
+// Scratch of lstm_forward_noalloc: the sync words (barrier counter, abort
+// word, per-XCD claim masks) that the persistent recurrences need, in a
+// device array each GPU holds until the process ends.  Host code never uses
+// the array's name as an address: its device address is looked up once per
+// device with hipGetSymbolAddress and kept in g_scratch_ptr.
+constexpr size_t NOALLOC_SCRATCH_BYTES = 64 * 1024;
+constexpr int MAX_DEVICES = 64;
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device (looked up on first use).
+lstm_status_t scratch_address(char **out)
+{
+    int dev = 0;
+    TRY_HIP("hipGetDevice", hipGetDevice(&dev));
+    if (dev < 0 || dev >= MAX_DEVICES) return invalid("device ordinal beyond the scratch table");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        TRY_HIP("hipGetSymbolAddress(scratch)", hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+        if (!ptr) return hip_status("hipGetSymbolAddress(scratch)", hipErrorInvalidSymbol);
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = static_cast<char *>(g_scratch_ptr[dev]);
+    return LSTM_OK;
+}
+}  // namespace
+
 extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
                                       const void *R, const float *b, const void *P, void *y, void *hT, float *cT,
                                       void *reserve, size_t reserve_bytes, void *workspace, size_t workspace_bytes,
                                       void *stream)
 {
     try {
-        if (!h) return invalid("handle is NULL");
-        const lstm_desc_t &d = h->d;
-        if (!x || !W || !R || !b || !y || !reserve || !workspace) return invalid("required pointer is NULL");
-        if ((P != nullptr) != (d.Hp > 0)) return invalid("P must be given iff Hp > 0");
-        for (const void *p : {x, h0, W, R, P, (const void *)y, (const void *)hT, (const void *)reserve, (const void *)workspace})
-            if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
-        for (const void *p : {(const void *)c0, (const void *)b, (const void *)cT})
-            if (p && !aligned4(p)) return invalid("fp32 tensors must be 4-byte aligned");
-        if (reserve_bytes < h->r_total) return short_buffer("reserve", reserve_bytes, h->r_total);
-        if (workspace_bytes < h->w_total) return short_buffer("workspace", workspace_bytes, h->w_total);
-        lstm_status_t st = ensure_plan(h);
+        lstm_status_t st = check_forward_args(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, reserve_bytes);
         if (st != LSTM_OK) return st;
-        hipStream_t s = static_cast<hipStream_t>(stream);
-        char *rv = static_cast<char *>(reserve);
-        char *wv = static_cast<char *>(workspace);
-        float *gates = reinterpret_cast<float *>(rv + h->r_gates);
+        if (!workspace) return invalid("required pointer is NULL");
+        if (!aligned16(workspace)) return invalid("device tensors must be 16-byte aligned");
+        if (workspace_bytes < h->w_total) return short_buffer("workspace", workspace_bytes, h->w_total);
+        st = ensure_plan(h);
+        if (st != LSTM_OK) return st;
+        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, static_cast<char *>(workspace),
+                            static_cast<hipStream_t>(stream));
+    } catch (...) {
+        return invalid("exception");
+    }
+}
 
+extern "C" lstm_status_t lstm_forward_noalloc(lstm_handle_t h, const void *x, const void *h0, const float *c0,
+                                              const void *W, const void *R, const float *b, const void *P, void *y,
+                                              void *hT, float *cT, void *reserve, size_t reserve_bytes, void *stream)
+{
+    try {
+        lstm_status_t st = check_forward_args(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, reserve_bytes);
+        if (st != LSTM_OK) return st;
+        st = ensure_plan(h);
+        if (st != LSTM_OK) return st;
+        // the persistent recurrences need only the sync words; the stepwise
+        // sequence (wide LSTMP layers) needs split-K partials as well
+        const lstm_desc_t &d = h->d;
         RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, h->ldy};
-        FwdBufs fb{};
-        fb.R = R; fb.P = P; fb.h0 = h0; fb.c0 = c0;
-        fb.gates = gates;
-        fb.cs = reinterpret_cast<float *>(rv + h->r_cs);
-        fb.ms = d.Hp ? rv + h->r_ms : nullptr;
-        fb.y = y; fb.hT = hT; fb.cT = cT;
-        fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
-        const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
-
-        GemmDesc g{};
-        g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
-        g.M = (int)h->TB; g.N = (int)h->G4; g.K = d.I;
-        g.A = x; g.lda = h->ldx;
-        g.B = W; g.ldb = d.I;
-        g.C = gates; g.ldc = h->G4;
-        g.bias = b; g.beta = 0;
-        if (xcd) g.side = xcd_prep_forward(sh, fb);   // the recurrence's exchange rows and flags
-        TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
-
-        if (!xcd && use_stepwise(h, h->fwd_ok)) {
-            StepwiseArgs sw{R, P, reinterpret_cast<float *>(wv + h->w_split), h->split_floats};
-            TRY_HIP("forward recurrence (stepwise)", forward_stepwise(h->dt, sh, fb, sw, s));
-        } else if (xcd) {
-            TRY_HIP("forward recurrence (XCD-local)", launch_forward_xcd(sh, fb, watchdog_ticks(), s, true));
-        } else {
-            TRY_HIP("forward recurrence", launch_forward(h->dt, sh, h->fwd, fb, s));
+        const bool stepwise = !xcd_path_ok(h->dt, sh, h->num_cus) && use_stepwise(h, h->fwd_ok);
+        const size_t need = stepwise ? h->w_split + h->split_floats * 4 : h->w_sync + SYNC_BYTES;
+        if (need > NOALLOC_SCRATCH_BYTES) {
+            std::snprintf(g_detail, sizeof(g_detail),
+                          "lstm_forward_noalloc: this layer needs %zu bytes of scratch, the library holds %zu "
+                          "(call lstm_forward with a workspace)", need, NOALLOC_SCRATCH_BYTES);
+            return LSTM_ERR_WORKSPACE;
         }
-        return LSTM_OK;
+        char *wv = nullptr;
+        st = scratch_address(&wv);
+        if (st != LSTM_OK) return st;
+        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, wv, static_cast<hipStream_t>(stream));
     } catch (...) {
         return invalid("exception");
     }
@@ -654,7 +741,8 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
 
 extern "C" lstm_status_t lstm_check(lstm_handle_t h, void *workspace, void *stream)
 {
-    if (!h || !workspace) return invalid("handle/workspace is NULL");
+    (void)workspace;   // the trip flags are per device, not per workspace
+    if (!h) return invalid("handle is NULL");
     hipStream_t s = static_cast<hipStream_t>(stream);
     TRY_HIP("stream sync", hipStreamSynchronize(s));
     unsigned tripped = 0;

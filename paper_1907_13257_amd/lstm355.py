@@ -57,6 +57,7 @@ def load_library():
         "lstm_workspace_size": ([H], sz),
         "lstm_forward": ([H] + [vp] * 11 + [sz, vp, sz, vp], i),
         "lstm_backward": ([H] + [vp] * 11 + [sz] + [vp] * 7 + [i, vp, sz, vp], i),
+        "lstm_forward_noalloc": ([H] + [vp] * 11 + [sz, vp], i),
         "lstm_forward_stack": ([i] + [vp] * 7 + [sz, vp, sz, vp], i),
         "lstm_backward_stack": ([i] + [vp] * 7 + [sz] + [vp] * 4 + [i, vp, sz, vp], i),
         "lstm_backward_stack_workspace_size": ([i, vp], sz),
@@ -143,6 +144,13 @@ def lstm_forward(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, workspace, stream
                                        _ptr(hT), _ptr(cT), _ptr(reserve), _nbytes(reserve, reserve_bytes),
                                        _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream)),
            "lstm_forward")
+
+
+def lstm_forward_noalloc(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, stream=None, reserve_bytes=None):
+    _check(load_library().lstm_forward_noalloc(h, _ptr(x), _ptr(h0), _ptr(c0), _ptr(W), _ptr(R), _ptr(b), _ptr(P),
+                                               _ptr(y), _ptr(hT), _ptr(cT), _ptr(reserve),
+                                               _nbytes(reserve, reserve_bytes), _stream(stream)),
+           "lstm_forward_noalloc")
 
 
 def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=None) -> bool:

@@ -197,3 +197,22 @@ def test_add_validates(lib):
 def test_profile_api_without_records(lib):
     L.lstm_profile_reset()
     assert L.lstm_profile_read() == {}
+
+
+def test_noalloc_forward_validates_before_launch(lib):
+    """lstm_forward_noalloc checks its arguments and the reserve's size on
+    the host, like lstm_forward, before anything touches the GPU."""
+    A = 1 << 20
+    h = L.lstm_create(4, 3, 32, 16, 0, "bf16")
+    R = L.lstm_reserve_size(h)
+
+    def call(x=A, P=None, rb=R):
+        return lib.lstm_forward_noalloc(h, x, None, None, A, A, A, P, A, None, None, A, rb, None)
+
+    assert call(x=None) == L.LSTM_ERR_INVALID_ARG
+    assert call(P=A) == L.LSTM_ERR_INVALID_ARG
+    assert call(x=A + 2) == L.LSTM_ERR_INVALID_ARG
+    assert call(rb=R - 1) == L.LSTM_ERR_WORKSPACE
+    assert lib.lstm_forward_noalloc(None, A, None, None, A, A, A, None, A, None, None, A, R, None) \
+        == L.LSTM_ERR_INVALID_ARG
+    L.lstm_destroy(h)
