@@ -397,9 +397,20 @@ __device__ __forceinline__ void tile_of(const GemmArgs &g, int lin, int &tm, int
 // GT: fused cell update (GemmDesc::cell_h): tile columns are cell-major gates
 // (column n is gate n % 4 of cell n / 4), and the epilogue applies the cell
 // equations to the four gates of each (row, cell) through LDS.
+// Four-wave configurations whose stages leave room for two workgroups per CU
+// are compiled for two (at most 256 registers per wave, accumulators and
+// operands together); otherwise the compiler may spend up to 512 and a CU
+// then holds one workgroup, one wave per SIMD.
+template <int BM, int BN, int KD, int NS, int NW>
+constexpr int dl_min_blocks()
+{
+    return (NW == 4 && NS * (BM + BN) * KD * 2 <= 80 * 1024) ? 2 : 1;
+}
+
 template <typename TO, int BM, int BN, bool AK, bool BKM, int KD, int NS, int NWM, int NWN, bool CB = false,
           bool GT = false>
-__global__ __launch_bounds__(64 * NWM * NWN, 1) void gemm_dl_kernel(GemmArgs g)
+__global__ __launch_bounds__(64 * NWM * NWN, (dl_min_blocks<BM, BN, KD, NS, NWM * NWN>()))
+void gemm_dl_kernel(GemmArgs g)
 {
     if (g.nbatch > 1) {   // product blockIdx.z of a batch (product 0's pointers are g's own)
         // constant indices keep the arguments in scalar registers
@@ -819,19 +830,24 @@ struct Choice {
 //  12: 256x128, 2x2, 32, 3     13: 128x256, 2x4, 64, 3   14: 256x128, 4x2, 64, 3
 //  15: 128x128, 2x2, 64, 3     16: 128x128, 2x2, 64, 4   17: 128x128, 2x2, 32, 8
 //  18: 64x128, 2x2, 64, 3       19: 64x64, 2x2, 64, 4     20: 128x64, 2x2, 64, 3
+//  21: 256x256, 4x4, 32, 4     22: 256x256, 4x4, 64, 2   23: 256x128, 4x4, 64, 3
+//  24: 128x256, 4x4, 64, 3
 // (16 and 17 keep 96 / 112 KiB of operands in flight per workgroup: the
 // per-step recurrent products stream their weights from HBM once; 18-20
-// give the skinny per-step products more workgroups.  An operand whose rows
+// give the skinny per-step products more workgroups; 21-24 are one
+// workgroup of 16 waves per CU, which loads a third fewer operand bytes per
+// product than two 128x256 workgroups.  An operand whose rows
 // are the contiguous dimension needs 128 of them per tile: its LDS swizzle
 // spans 16 chunks of 16 bytes.)
-constexpr int NTILES = 21;
-const int kTileBM[NTILES] = {256, 256, 128, 128, 256, 128, 256, 128, 256, 256, 256,
-                             128, 256, 128, 256, 128, 128, 128, 64,  64,  128};
-const int kTileBN[NTILES] = {256, 128, 256, 128, 256, 128, 128, 256, 256, 256, 256,
-                             256, 128, 256, 128, 128, 128, 128, 128, 64,  64};
-const int kTileKD[NTILES] = {32, 32, 32, 32, 32, 64, 64, 64, 64, 32, 64, 32, 32, 64, 64, 64, 64, 32, 64, 64, 64};
+constexpr int NTILES = 25;
+const int kTileBM[NTILES] = {256, 256, 128, 128, 256, 128, 256, 128, 256, 256, 256, 128, 256,
+                             128, 256, 128, 128, 128, 64,  64,  128, 256, 256, 256, 128};
+const int kTileBN[NTILES] = {256, 128, 256, 128, 256, 128, 128, 256, 256, 256, 256, 256, 128,
+                             256, 128, 128, 128, 128, 128, 64,  64,  256, 256, 128, 256};
+const int kTileKD[NTILES] = {32, 32, 32, 32, 32, 64, 64, 64, 64, 32, 64, 32, 32,
+                             64, 64, 64, 64, 32, 64, 64, 64, 32, 64, 64, 64};
 // Workgroups of each configuration that fit on one CU (LDS-limited).
-const int kTileSlots[NTILES] = {1, 1, 1, 2, 1, 2, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, 1, 2, 2, 2};
+const int kTileSlots[NTILES] = {1, 1, 1, 2, 1, 2, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, 1, 2, 2, 2, 1, 1, 1, 1};
 
 bool dl_ok(const GemmDesc &d, int BM, int BN, int splits);
 bool tile_fits(const GemmDesc &d, int t);
@@ -902,6 +918,17 @@ Choice choose(const GemmDesc &d, size_t es)
         return Choice{18, model_splits(d, 64, 128, kTileSlots[18], kTileKD[18])};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
+    if (es == 2 && d.a_kmajor && d.b_kmajor && tile_fits(d, 22)) {
+        // both operands k-contiguous (the input projection) with enough
+        // 256x256 tiles to occupy most CUs: one 16-wave workgroup per CU
+        // loads a third fewer operand bytes from L2 per product than two
+        // 128x256 workgroups, the limit of those.  Measured: 6400 x 4096 x
+        // 1024 89 -> 74 us, 3200 rows 44 -> 38 us, 25600 rows 387 -> 321 us,
+        // K = 2048 339 -> 287 us, 2560 x 32768 x 1024 285 -> 237 us; with
+        // 1600 rows (112 tiles) 29.5 -> 34.6 us, so not below ~192 tiles.
+        const long tiles = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
+        if (tiles >= 192) return Choice{22, 1};
+    }
     if (es == 2 && d.a_kmajor && d.b_kmajor && dl_ok(d, 128, 256, 1)) {
         // both operands k-contiguous (the input projection): 128x256 tiles of
         // 8 waves move less L2 traffic per flop than 128x128 once they fill
@@ -1015,6 +1042,10 @@ hipError_t launch_tile(int tile, const GemmDesc &d, int splits, hipStream_t s)
     case 20:
         if constexpr (BKM) return launch_gemm_dl<TO, 128, 64, AK, BKM, 64, 3, 2, 2>(d, splits, s);
         return hipErrorInvalidValue;
+    case 21: return launch_gemm_dl<TO, 256, 256, AK, BKM, 32, 4, 4, 4>(d, splits, s);
+    case 22: return launch_gemm_dl<TO, 256, 256, AK, BKM, 64, 2, 4, 4>(d, splits, s);
+    case 23: return launch_gemm_dl<TO, 256, 128, AK, BKM, 64, 3, 4, 4>(d, splits, s);
+    case 24: return launch_gemm_dl<TO, 128, 256, AK, BKM, 64, 3, 4, 4>(d, splits, s);
     default: return launch_gemm_dl<TO, 128, 128, AK, BKM, 32, 4, 2, 2>(d, splits, s);
     }
 }

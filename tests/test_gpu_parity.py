@@ -127,6 +127,7 @@ LAYER_CASES = [
     (2, 1, 8, 1024, 0, "bf16", True),      # one row in all, full-width cells
     (3, 136, 64, 1024, 0, "bf16", False),  # full-width cells, 17 rows per XCD: two row blocks
     (3, 264, 64, 1024, 0, "bf16", True),   # full-width cells, 33 rows per XCD: four row blocks, reverse
+    (13, 250, 64, 1024, 0, "bf16", False), # input projection on 256x256 tiles (208 of them, ragged last row)
     # [dW | dR] as one product (bf16, B a multiple of 32, I and I + H multiples of 128)
     (4, 32, 128, 256, 0, "bf16", False),   # with h0: the first step's segment comes from h0
     (3, 64, 128, 256, 0, "bf16", True),    # reverse: h0 pairs with the last time index
@@ -140,7 +141,12 @@ XCD_VARIANT = 1000
 def test_layer_parity(T, B, I, H, Hp, dtype, reverse):
     label = f"layer T{T} B{B} I{I} H{H} Hp{Hp} {dtype} rev{int(reverse)}"
     announce(label)
-    c = layer_case(T, B, I, H, Hp, dtype, reverse, seed=T * 1000 + B)
+    # full-width cells get the networks' weight range, U(+-0.1): with
+    # U(+-0.3) the recurrence at H = 1024 has a gain of about 5 per step and is
+    # chaotic, so the bf16 rounding of h grows step by step (0.2% at the first
+    # step, 8% at the thirteenth) whatever the kernels do
+    scale = 0.3 if H < 1024 else 0.1
+    c = layer_case(T, B, I, H, Hp, dtype, reverse, seed=T * 1000 + B, scale=scale)
     gpu = run_layer_gpu(c, T, B, I, H, Hp, dtype, reverse)
     ref = oracle_layer(c, Hp, reverse)
     check_layer(gpu, ref, dtype, label)
