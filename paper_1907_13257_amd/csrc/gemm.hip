@@ -513,6 +513,11 @@ void gemm_dl_kernel(GemmArgs g)
         }
         const char *abase = smem + (st % NS) * STAGE;
         const char *bbase = abase + ABYTES;
+        // raised wave priority while the stage's products issue: the
+        // arbiter then favours waves with matrix work over waves issuing
+        // loads or waiting at the barrier ([dW | dR] at 4096 x 2048 x 6400:
+        // 128.7 -> 122.8 us, the other products unchanged)
+        __builtin_amdgcn_s_setprio(3);
 #pragma unroll
         for (int s = 0; s < KD / 16; ++s) {
             u32x4 fa[FM], fb[FN];
@@ -523,6 +528,7 @@ void gemm_dl_kernel(GemmArgs g)
 #pragma unroll
                 for (int j = 0; j < FN; ++j) mfma32(acc[i][j], fa[i], fb[j], bf16_t{});
         }
+        __builtin_amdgcn_s_setprio(0);
     }
 
     const bool split = g.partial != nullptr;
