@@ -51,12 +51,15 @@ def make_workload(args):
         return synth.biglstm(B=args.batch or 128)
     if args.workload == "gnmt8":
         return synth.gnmt8(B=args.batch or 256)
+    if args.workload == "floor":
+        return synth.floor(B=args.batch or 8)
     raise SystemExit(f"unknown workload {args.workload}")
 
 
 def workload_name(wl) -> str:
     L0 = wl.layers[0]
-    kinds = {"gnmt4": "gnmt4_lstm", "biglstm": "biglstm_lstmp", "gnmt8": "gnmt8_bi_residual_lstm"}
+    kinds = {"gnmt4": "gnmt4_lstm", "biglstm": "biglstm_lstmp", "gnmt8": "gnmt8_bi_residual_lstm",
+             "floor": "sync_floor_lstm"}
     base = kinds.get(wl.name.split("_B")[0], wl.name)
     hp = f"_P{L0.Hp}" if L0.Hp else ""
     return f"{base}_L{len(wl.layers)}_I{L0.I}_H{L0.H}{hp}_T{wl.T}_B{wl.B}"
@@ -175,13 +178,33 @@ def traffic_from(pmc_dir: str, workload: str, copy_mib: int):
         hits = [v for k, v in by_name.items() if k.startswith(prefixes)]
         if len(hits) == 1:
             kernels[cls] = {"hbm_bytes_per_launch": hits[0]}
-    out = {"source_hash": kernel_source_hash(), "workload": workload, "fetch_factor": fetch_factor,
-           "write_factor": write_factor, "copy_bytes": copy_mib * (1 << 20),
-           "kernels": kernels, "bytes_per_dispatch_by_kernel": by_name}
+    # one record per workload, all taken on the same kernel sources
+    out = {"source_hash": kernel_source_hash(), "workloads": {}}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            old = json.load(f)
+        if old.get("source_hash") == out["source_hash"]:
+            out["workloads"] = old.get("workloads", {})
+    out["workloads"][workload] = {"fetch_factor": fetch_factor, "write_factor": write_factor,
+                                  "copy_bytes": copy_mib * (1 << 20), "kernels": kernels,
+                                  "bytes_per_dispatch_by_kernel": by_name}
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
-    print(json.dumps({"traffic_file": TRAFFIC_FILE, "kernels": kernels, "fetch_factor": fetch_factor,
-                      "write_factor": write_factor}))
+    print(json.dumps({"traffic_file": TRAFFIC_FILE, "workload": workload, "kernels": kernels,
+                      "fetch_factor": fetch_factor, "write_factor": write_factor}))
+
+
+def traffic_for(workload: str, cls: str):
+    """HBM bytes per launch of kernel class `cls` counted for `workload` on the
+    current kernel sources, or None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        tr = json.load(f)
+    if tr.get("source_hash") != kernel_source_hash():
+        return None
+    ent = tr.get("workloads", {}).get(workload, {}).get("kernels", {}).get(cls)
+    return ent.get("hbm_bytes_per_launch") if ent else None
 
 
 def main():
@@ -189,7 +212,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="gnmt4", choices=["gnmt4", "biglstm", "gnmt8"])
+    ap.add_argument("--workload", default="gnmt4", choices=["gnmt4", "biglstm", "gnmt8", "floor"])
     ap.add_argument("--batch", type=int, default=0)
     ap.add_argument("--cpu-rows", type=int, default=16, help="batch rows for the oracle baseline (0: skip)")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
@@ -307,13 +330,7 @@ def main():
         dom = max(stats, key=lambda k: stats[k]["total_ms"])
         s = stats[dom]
         avg_s = s["total_ms"] / s["launches"] / 1e3
-        traffic = None
-        if os.path.exists(TRAFFIC_FILE):
-            with open(TRAFFIC_FILE) as f:
-                tr = json.load(f)
-            ent = tr.get("kernels", {}).get(dom)
-            if ent and tr.get("source_hash") == kernel_source_hash() and tr.get("workload") == workload_name(wl):
-                traffic = ent.get("hbm_bytes_per_launch")
+        traffic = traffic_for(workload_name(wl), dom)
         if dom in GEMM_CLASSES:
             ach = s["flops"] / s["launches"] / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",

@@ -153,6 +153,13 @@ def gnmt8(T: int = 50, B: int = 256) -> Workload:
     return Workload("gnmt8_bi_residual", T=T, B=B, layers=layers, dtype="bf16", seed=4, w_scale=0.1)
 
 
+def floor(T: int = 50, B: int = 8) -> Workload:
+    """The smallest layer the XCD-local recurrences take (256 cells, one batch
+    row per XCD): its per-step time is the kernels' exchange and
+    synchronisation floor, with almost no arithmetic or traffic per step."""
+    return Workload(f"floor_B{B}", T=T, B=B, layers=[LayerSpec(256, 256)], dtype="bf16", seed=5, w_scale=0.1)
+
+
 CONFIGS = {
     "tiny": tiny,
     "gnmt4": gnmt4,
