@@ -120,12 +120,19 @@ lstm_status_t lstm_forward_noalloc(lstm_handle_t h,
  * the paper uses for model parallelism of GNMT and BigLSTM (Section 2,
  * "Background"; Section 4, "Model Parallel Splitting"), here spread over the
  * XCDs of one GPU.  The result equals L calls of lstm_forward with
- * x_{l+1} = y_l, zero initial states and no final states.
+ * x_{l+1} = y_l (or y_l + x_l for a residual layer, see below), zero initial
+ * states and no final states.
  *   h[l]: handles of the layers (bf16, Hp = 0, not reversed, equal T, B, H;
  *     layer l >= 1 has I = H and dense x and y).
  *   x: the stack's input, as for lstm_forward on h[0].
  *   W[l], R[l], b[l]: parameters of layer l.
  *   y[l]: output of layer l [T][B][H] (the input of layer l+1).
+ *   residual: NULL, or per layer 0/1; residual[l] = 1 makes layer l's output
+ *     y[l] + (its input), the residual connection of the GNMT encoder
+ *     (Section 4, "Model Parallel Splitting"); that sum, the input of layer
+ *     l+1 (or the stack's output for the top layer), goes to ysum[l]
+ *     [T][B][H].  A residual layer needs an input as wide as its output.
+ *     The sums are rounded to bf16 as lstm_add rounds them.
  *   reserve[l]: reserve of layer l (lstm_reserve_size(h[l]) bytes), for
  *     lstm_backward on h[l] exactly as after lstm_forward; reserve_bytes is
  *     the size of each of them.
@@ -136,7 +143,8 @@ lstm_status_t lstm_forward_noalloc(lstm_handle_t h,
  * call may have written). */
 lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *h, const void *x,
                                  const void *const *W, const void *const *R, const float *const *b,
-                                 void *const *y, void *const *reserve, size_t reserve_bytes,
+                                 void *const *y, const int *residual, void *const *ysum,
+                                 void *const *reserve, size_t reserve_bytes,
                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /* Back-propagation through time for the loss
@@ -167,9 +175,13 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  * of one after another; the weight gradients follow per layer.  The result
  * equals lstm_backward on each layer from the top down, with dy of layer l-1
  * = dx of layer l, zero initial states and no gradient for the final states.
- *   h[l], W[l], R[l], y[l], reserve[l], reserve_bytes: as given to lstm_forward_stack
- *     (every layer with I = H: the stack's input x has the layers' width).
- *   dy: gradient of the top layer's output y[L-1], [T][B][H].
+ *   h[l], W[l], R[l], y[l], residual, ysum[l], reserve[l], reserve_bytes: as
+ *     given to lstm_forward_stack (every layer with I = H: the stack's input
+ *     x has the layers' width).  A residual layer's upstream gradient also
+ *     reaches its input unchanged: the input gradient of layer l is dz_l W_l
+ *     plus the gradient of layer l's output.
+ *   dy: gradient of the stack's output (y[L-1], or ysum[L-1] when the top
+ *     layer is residual), [T][B][H].
  *   x: the stack's input (layer 0's input).
  *   dx: gradient of x [T][B][H], NULL when not wanted.
  *   dW[l], dR[l], db[l]: fp32 weight gradients of layer l; accumulate as for
@@ -182,6 +194,7 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  * caller runs lstm_backward layer by layer. */
 lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *h, const void *dy, const void *x,
                                   const void *const *W, const void *const *R, const void *const *y,
+                                  const int *residual, const void *const *ysum,
                                   const void *const *reserve, size_t reserve_bytes, void *dx,
                                   float *const *dW, float *const *dR, float *const *db, int accumulate,
                                   void *workspace, size_t workspace_bytes, void *stream);

@@ -341,8 +341,9 @@ extern "C" lstm_status_t lstm_forward_noalloc(lstm_handle_t h, const void *x, co
 
 extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, const void *x, const void *const *W,
                                             const void *const *R, const float *const *b, void *const *y,
-                                            void *const *reserve, size_t reserve_bytes, void *workspace,
-                                            size_t workspace_bytes, void *stream)
+                                            const int *residual, void *const *ysum, void *const *reserve,
+                                            size_t reserve_bytes, void *workspace, size_t workspace_bytes,
+                                            void *stream)
 {
     try {
         if (L < 1 || !hs || !x || !W || !R || !b || !y || !reserve || !workspace)
@@ -354,6 +355,15 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
             if (!aligned4(b[l])) return invalid("fp32 tensors must be 4-byte aligned");
         }
         if (!aligned16(x) || !aligned16(workspace)) return invalid("device tensors must be 16-byte aligned");
+        if (residual)
+            for (int l = 0; l < L; ++l)
+                if (residual[l]) {
+                    if (!ysum || !ysum[l]) return invalid("a residual layer needs its sum buffer");
+                    if (!aligned16(ysum[l])) return invalid("device tensors must be 16-byte aligned");
+                    const lstm_desc_t &d = hs[l]->d;
+                    if (d.I != d.H || hs[l]->ldx != d.H || hs[l]->ldy != d.H)
+                        return invalid("a residual layer needs an input as wide as its output");
+                }
         for (int l = 0; l < L; ++l) {
             if (reserve_bytes < hs[l]->r_total) return short_buffer("reserve", reserve_bytes, hs[l]->r_total);
             if (workspace_bytes < hs[l]->w_total) return short_buffer("workspace", workspace_bytes, hs[l]->w_total);
@@ -389,7 +399,20 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
             wb[l].gates = reinterpret_cast<float *>(rv + hs[l]->r_gates);
             wb[l].cs = reinterpret_cast<float *>(rv + hs[l]->r_cs);
             wb[l].y = y[l];
+            wb[l].in_b = nullptr;
+            wb[l].sum = nullptr;
+            wb[l].poll_b = 0;
         }
+        // output of layer l (the input of layer l+1): y_l, or y_l plus the
+        // layer's own input for a residual layer
+        auto res = [&](int l) { return residual && residual[l]; };
+        auto input_of = [&](int l) -> const void * { return l == 0 ? x : (res(l - 1) ? ysum[l - 1] : y[l - 1]); };
+        for (int l = 1; l < L; ++l)
+            if (res(l - 1)) {   // layer l's projection forms the sum and stores it
+                wb[l].in_b = input_of(l - 1);
+                wb[l].poll_b = l - 1 > 0;
+                wb[l].sum = ysum[l - 1];
+            }
         // Layer 0's input projection: inside the wavefront when x has the
         // layers' width (an otherwise idle XCD computes it step by step),
         // else by the GEMM as in lstm_forward.  The other layers' are always
@@ -409,6 +432,9 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
         TRY_HIP("layer wavefront", launch_forward_wave(sh, L, x_in_wave ? x : nullptr, wb,
                                                        reinterpret_cast<unsigned *>(wv + h0->w_sync),
                                                        watchdog_ticks(), s));
+        if (res(L - 1))   // the top layer's sum: the stack's output
+            TRY_HIP("residual sum", add(DType::BF16, (size_t)d0.T * d0.B * d0.H, y[L - 1], input_of(L - 1),
+                                        ysum[L - 1], s));
         return LSTM_OK;
     } catch (...) {
         return invalid("exception");
@@ -472,6 +498,7 @@ extern "C" size_t lstm_backward_stack_workspace_size(int L, const lstm_handle_t 
 
 extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, const void *dy, const void *x,
                                              const void *const *W, const void *const *R, const void *const *y,
+                                             const int *residual, const void *const *ysum,
                                              const void *const *reserve, size_t reserve_bytes, void *dx,
                                              float *const *dW, float *const *dR, float *const *db, int accumulate,
                                              void *workspace, size_t workspace_bytes, void *stream)
@@ -490,6 +517,10 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
         }
         for (const void *p : {dy, x, (const void *)dx, (const void *)workspace})
             if (p && !aligned16(p)) return invalid("device tensors must be 16-byte aligned");
+        auto res = [&](int l) { return residual && residual[l]; };
+        for (int l = 0; l < L - 1; ++l)   // the sums that feed the layers above (the weight gradients' inputs)
+            if (res(l) && (!ysum || !ysum[l] || !aligned16(ysum[l])))
+                return invalid("a residual layer needs its 16-byte aligned sum buffer");
         if (const char *why = stack_bwd_unfit(L, hs)) {
             std::snprintf(g_detail, sizeof(g_detail), "layer wavefront not available: %s", why);
             return LSTM_ERR_UNSUPPORTED;
@@ -522,7 +553,7 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
             g.in = DType::BF16; g.out_f32 = true; g.a_kmajor = false; g.b_kmajor = false;
             g.M = (int)G4; g.N = 2 * H; g.K = (int)TB;
             g.A = wv + lay.dz[l]; g.lda = G4;
-            g.B = l == 0 ? x : y[l - 1]; g.ldb = H;
+            g.B = l == 0 ? x : (res(l - 1) ? ysum[l - 1] : y[l - 1]); g.ldb = H;
             g.C = dW[l]; g.ldc = H; g.beta = accumulate;
             g.N1 = H;
             g.B2 = y[l]; g.ldb2 = H; g.b2_bytes = TB * H * 2;   // dz_t pairs with y_{t-1}; h0 is zero
@@ -559,6 +590,7 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
             wb[l].dy_fill = l == L - 1 ? nullptr : wv + lay.dy[l];
             wb[l].dx = l == 0 ? dx : wv + lay.dy[l - 1];
             wb[l].dbp = reinterpret_cast<float *>(wv + lay.dbp) + (size_t)l * G4;
+            wb[l].residual = res(l) ? 1 : 0;
         }
         // one launch transposes R and W of every layer and arms the rows the
         // wavefront exchanges; then the wavefront itself

@@ -115,11 +115,12 @@ bool gemm_dual_ok(const GemmDesc &d);
 // dst[c][r] = src[r][c]; `side` (optional) is done by the same launch.
 hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hipStream_t s,
                      const SideJob *side = nullptr);
-// Up to 9 word ranges, each filled with its own value: p[r][0..n[r]) = v[r].
+// Up to FILL_MAX word ranges, each filled with its own value: p[r][0..n[r]) = v[r].
+constexpr int FILL_MAX = 16;
 struct FillRanges {
-    uint32_t *p[9];
-    long n[9];
-    uint32_t v[9];
+    uint32_t *p[FILL_MAX];
+    long n[FILL_MAX];
+    uint32_t v[FILL_MAX];
     int count;
 };
 // n (1..8) 16-bit matrices of one shape [rows][cols] (multiples of 64,
@@ -243,6 +244,12 @@ struct WaveBufs {
     const float *bias;
     float *gates, *cs;
     void *y;
+    // the layer below is residual: this layer's input is y of the layer below
+    // plus in_b (written in the launch when poll_b), formed by this layer's
+    // projection and stored into `sum`; NULL / 0 otherwise
+    const void *in_b;
+    void *sum;
+    int poll_b;
 };
 bool wave_path_ok(const RecShape &sh, int num_cus);
 hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const WaveBufs *ly, unsigned *sync,
@@ -260,6 +267,7 @@ struct WaveBwdBufs {
     void *dy_fill;   // dy when the launch writes it (layers below the top), else NULL
     void *dx;
     float *dbp;
+    int residual;    // the layer's output is y + its input: dx also receives dy (the identity path)
 };
 // The fills launch_backward_wave needs before its launch (flags, dz, the
 // upstream gradients written inside the launch); with `prefilled` the caller

@@ -376,7 +376,7 @@ hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, 
 {
     if (n < 1 || n > 8 || rows % 64 || cols % 64) return hipErrorInvalidValue;
     const FillRanges f = fill ? *fill : FillRanges{};
-    if (f.count < 0 || f.count > 9) return hipErrorInvalidValue;
+    if (f.count < 0 || f.count > FILL_MAX) return hipErrorInvalidValue;
     TransposeBatch b{};
     for (int i = 0; i < n; ++i) {
         if (((reinterpret_cast<uintptr_t>(src[i]) | reinterpret_cast<uintptr_t>(dst[i])) & 15) != 0)

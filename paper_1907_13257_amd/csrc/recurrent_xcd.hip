@@ -213,6 +213,94 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
     }
 }
 
+// a + b of eight bf16 pairs, in fp32, rounded to bf16 as the element-wise
+// add kernel rounds them (a result equal to NOT_READY becomes the canonical
+// NaN, as for every exchanged value).
+__device__ __forceinline__ u32x4 bf16_add8(u32x4 a, u32x4 b)
+{
+    u32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float lo = __uint_as_float(a[i] << 16) + __uint_as_float(b[i] << 16);
+        const float hi = __uint_as_float(a[i] & 0xffff0000u) + __uint_as_float(b[i] & 0xffff0000u);
+        r[i] = (unsigned)ready_value(f32_to_bf16(lo)) | ((unsigned)ready_value(f32_to_bf16(hi)) << 16);
+    }
+    return r;
+}
+
+// The residual form of stage_mma_when_ready: the rows multiplied are the sums
+// a + b of two row sets (a residual layer's output y + x), each either
+// exchanged (poll_*: copied with loads that miss L1 and repeated while an
+// element of a valid row holds NOT_READY) or complete before the launch.
+// Once every element is final and `store` is set, the wave also stores its
+// slice of the summed rows into `rsum` with device-coherent stores (one
+// workgroup per XCD stores them; each element is written once).
+template <int RB, int KCW, int NBX>
+__device__ __forceinline__ bool stage_sum_mma_when_ready(u32x4 rsa, u32x4 rsb, bool poll_a, bool poll_b, long r0,
+                                                         long ld, int kbyte, unsigned tile_a, const char *tpa,
+                                                         unsigned tile_b, const char *tpb, int lane, int valid,
+                                                         const u32x4 (&rf)[NBX][KCW], f32x4 (&acc)[NBX],
+                                                         __amdgpu_buffer_rsrc_t rsum, bool store, unsigned *flags,
+                                                         unsigned long long timeout)
+{
+    constexpr int RPI = 1024 / RB > 0 ? 1024 / RB : 1;
+    static_assert(RB <= 1024, "one row per instruction at most");
+    const __amdgpu_buffer_rsrc_t rfl = rsrc(flags);
+    const bool row_in = (lane & 15) < valid;
+    const unsigned long long t0 = wall_clock64();
+    unsigned qmask = 0;
+#pragma unroll
+    for (int q = 0; q < 16 / RPI; ++q)
+        if (q * RPI < valid) qmask |= 1u << q;
+    while (true) {
+        if (poll_a)
+            stage_rows<RB, true>(rsa, r0, ld, kbyte, tile_a, lane, qmask);
+        else
+            stage_rows<RB, false>(rsa, r0, ld, kbyte, tile_a, lane, qmask);
+        if (poll_b)
+            stage_rows<RB, true>(rsb, r0, ld, kbyte, tile_b, lane, qmask);
+        else
+            stage_rows<RB, false>(rsb, r0, ld, kbyte, tile_b, lane, qmask);
+        const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+        wait_own_loads();
+#pragma unroll
+        for (int i = 0; i < NBX; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        u16x2 seen = {0, 0};
+#pragma unroll
+        for (int c = 0; c < KCW; ++c) {
+            const u32x4 fa = stage_frag<RB>(tpa, c, lane);
+            const u32x4 fb = stage_frag<RB>(tpb, c, lane);
+            if (poll_a) seen = max_halves(seen, fa);
+            if (poll_b) seen = max_halves(seen, fb);
+            const u32x4 fs = bf16_add8(fa, fb);
+#pragma unroll
+            for (int i = 0; i < NBX; ++i) mfma16(acc[i], rf[i][c], fs, bf16_t{});
+        }
+        const unsigned long long lm = __builtin_amdgcn_ballot_w64(saw_not_ready(seen) && row_in);
+        if (lm == 0) {
+            if (store && row_in) {   // lane: row lane % 16, k = c*32 + (lane/16)*8 .. +7 of the wave's slice
+#pragma unroll
+                for (int c = 0; c < KCW; ++c) {
+                    const u32x4 fs = bf16_add8(stage_frag<RB>(tpa, c, lane), stage_frag<RB>(tpb, c, lane));
+                    const unsigned off =
+                        (unsigned)(((r0 + (lane & 15)) * ld) * 2 + kbyte + c * 64 + (lane >> 4) * 16);
+                    __builtin_amdgcn_raw_buffer_store_b128(fs, rsum, off, 0, 16);
+                }
+            }
+            return true;
+        }
+        if (ab != 0) return false;
+        if (wall_clock64() - t0 > timeout) {
+            if (lane == 0) {
+                __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            return false;
+        }
+        wait_own_lds();
+    }
+}
+
 struct XFwdArgs {
     int T, B, H, reverse, RX;
     long ldy;
@@ -387,6 +475,12 @@ struct WaveLayer {
     const float *bias;
     float *gates, *cs;   // gates: the input projection in, the activations out
     bf16_t *y;           // [T][B][H]
+    // residual input (the layer below adds its own input to its output): the
+    // projection multiplies y of the layer below plus in_b, and stores that
+    // sum into `sum`; poll_b: in_b is written in the launch
+    const bf16_t *in_b;
+    bf16_t *sum;
+    int poll_b;
 };
 
 struct XWaveArgs {
@@ -405,7 +499,7 @@ __device__ __forceinline__ unsigned ready_f32(float v)
     return u == NOT_READY_F32 ? 0x7fc00000u : u;
 }
 
-template <int HN, int MBX>
+template <int HN, int MBX, bool RES = false>
 __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
 {
     constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
@@ -417,6 +511,7 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
     constexpr int RP = NT + 36;
     __shared__ __attribute__((aligned(16))) float red[8][16][RP];
     __shared__ __attribute__((aligned(1024))) char stage[8][16 * RB];
+    __shared__ __attribute__((aligned(1024))) char stage_b[RES ? 8 : 1][RES ? 16 * RB : 16];   // second addend
     __shared__ int s_xcd;
     __shared__ int s_bad;
 
@@ -476,6 +571,17 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
 #pragma unroll
                         for (int i = 0; i < NB; ++i) mfma16(acc[i], rf[i][c], fa, bf16_t{});
                     }
+                } else if (RES && ly.in_b) {   // the layer below is residual: multiply y + its input
+                    if (mb > 0) wait_own_lds();
+                    const u32x4 rs_b = buffer_desc(ly.in_b, (long)a.T * B * H * 2);
+                    const __amdgpu_buffer_rsrc_t rsum =
+                        __builtin_amdgcn_make_buffer_rsrc(ly.sum, (short)0, (int)((long)a.T * B * H * 2), 0x00020000);
+                    if (!stage_sum_mma_when_ready<RB, KCW, NB>(rs_x, rs_b, true, ly.poll_b != 0, (long)s * B + rb0, H,
+                                                               w * KW * 2, tile, stage[w],
+                                                               lds_addr(&stage_b[RES ? w : 0][0]),
+                                                               stage_b[RES ? w : 0], lane, B - rb0, rf, acc, rsum,
+                                                               slot == 0, a.flags, a.timeout))
+                        s_bad = 1;
                 } else {
                     if (mb > 0) wait_own_lds();
                     if (!stage_mma_when_ready<RB, KCW, NB, true>(rs_x, (long)s * B + rb0, H, w * KW * 2, tile,
@@ -618,6 +724,8 @@ struct WaveBwdLayer {
     const bf16_t *dy;          // [T][B][H] upstream gradient (for l < L-1 written by XCD 2l+3)
     bf16_t *dx;                // [T][B][H] input gradient (dy of layer l-1, or the stack's dx)
     float *dbp;                // [4H] bias gradient of layer l
+    const bf16_t *dres;        // residual layer: its upstream gradient, added to dx (the identity path)
+    int poll_res;              // dres is written in the launch
 };
 
 struct XWaveBwdArgs {
@@ -627,7 +735,7 @@ struct XWaveBwdArgs {
     unsigned long long timeout;
 };
 
-template <int HN, int MBX>
+template <int HN, int MBX, bool RES = false>
 __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
 {
     constexpr int NBB = HN / 16;
@@ -689,14 +797,45 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
                     for (int v = 0; v < 4; ++v) red[w][4 * (lane >> 4) + v][i * 16 + (lane & 15)] = acc[i][v];
                 __syncthreads();
                 if (s_bad) return;
-                if (has_cell && rb0 + cr < B) {
+                const bool vr = has_cell && rb0 + cr < B;
+                // residual layer: its upstream gradient also reaches its input unchanged
+                bf16_t g = 0;
+                if (RES && ly.dres) {
+                    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+                        const_cast<bf16_t *>(ly.dres), (short)0, (int)((long)T * B * H * 2), 0x00020000);
+                    const unsigned off = (unsigned)((((long)s * B + rb0 + crr) * H + cj) * 2);
+                    if (vr)   // sc1 (16): the rows written in the launch are read past L1
+                        g = ly.poll_res ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 16)
+                                        : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 0);
+                    if (ly.poll_res) {
+                        const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
+                        const unsigned long long t0 = wall_clock64();
+                        while (__builtin_amdgcn_ballot_w64(vr && g == NOT_READY) != 0) {
+                            const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+                            if (ab != 0 || wall_clock64() - t0 > a.timeout) {
+                                if (lane == 0 && ab == 0) {
+                                    __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT);
+                                    __hip_atomic_store(a.flags + XCD_ABORT, 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                                }
+                                s_bad = 1;
+                                break;
+                            }
+                            if (vr && g == NOT_READY) g = (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 16);
+                        }
+                    }
+                }
+                if (vr) {
                     float v = 0.0f;
 #pragma unroll
                     for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
+                    if (RES && ly.dres) v += to_f32(g);
                     __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(v)), rdx,
                                                           (unsigned)((((long)s * B + rb0 + cr) * H + cj) * 2), 0, 16);
                 }
                 __syncthreads();   // red is rewritten by the next block or step
+                if (RES && s_bad) return;
             }
         }
         return;
@@ -1095,6 +1234,10 @@ FillRanges forward_wave_fills(const RecShape &sh, int L, const void *x, const Wa
             f.p[nr] = reinterpret_cast<uint32_t *>(ly[l].gates); f.n[nr] = rows * 4 * sh.H;
             f.v[nr++] = NOT_READY_F32;
         }
+        if (ly[l].sum) {   // residual sums formed in the launch (a layer above may poll them)
+            f.p[nr] = static_cast<uint32_t *>(ly[l].sum); f.n[nr] = rows * sh.H / 2;
+            f.v[nr++] = ((uint32_t)NOT_READY << 16) | NOT_READY;
+        }
     }
     f.count = nr;
     return f;
@@ -1108,6 +1251,7 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
     XWaveArgs a{};
     a.T = sh.T; a.B = sh.B; a.H = sh.H; a.L = L;
     a.x = static_cast<const bf16_t *>(x);
+    bool res = false;
     for (int l = 0; l < L; ++l) {
         a.ly[l].R = static_cast<const bf16_t *>(ly[l].R);
         a.ly[l].W = static_cast<const bf16_t *>(ly[l].W);
@@ -1115,6 +1259,13 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
         a.ly[l].gates = ly[l].gates;
         a.ly[l].cs = ly[l].cs;
         a.ly[l].y = static_cast<bf16_t *>(ly[l].y);
+        a.ly[l].in_b = static_cast<const bf16_t *>(ly[l].in_b);
+        a.ly[l].sum = static_cast<bf16_t *>(ly[l].sum);
+        a.ly[l].poll_b = ly[l].poll_b;
+        if (ly[l].in_b) {
+            if (l == 0 || !ly[l].sum) return hipErrorInvalidValue;   // a sum is formed from the layer below
+            res = true;
+        }
     }
     a.flags = sync + XCD_FLAGS;
     a.timeout = timeout;
@@ -1133,6 +1284,10 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + np),
                  (double)L * (sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0) +
                      np * ((double)sh.T * sh.B * (G4 * 4.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
+    if (res) {
+        if (sh.B <= 16) return launch256<lstm_fwd_wave<32, 1, true>>(s, &a);
+        return launch256<lstm_fwd_wave<32, 2, true>>(s, &a);
+    }
     if (sh.B <= 16) return launch256<lstm_fwd_wave<32, 1>>(s, &a);
     return launch256<lstm_fwd_wave<32, 2>>(s, &a);
 }
@@ -1160,6 +1315,7 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
     if (L < 2 || L > 4) return hipErrorInvalidValue;
     XWaveBwdArgs a{};
     a.T = sh.T; a.B = sh.B; a.H = sh.H; a.L = L;
+    bool res = false;
     for (int l = 0; l < L; ++l) {
         a.ly[l].Rt = static_cast<const bf16_t *>(ly[l].Rt);
         a.ly[l].Wt = static_cast<const bf16_t *>(ly[l].Wt);
@@ -1169,6 +1325,11 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
         a.ly[l].dy = static_cast<const bf16_t *>(ly[l].dy);
         a.ly[l].dx = static_cast<bf16_t *>(ly[l].dx);
         a.ly[l].dbp = ly[l].dbp;
+        // a residual layer's input gradient adds its upstream gradient, which
+        // the layer above writes in the launch (the stack's own for the top layer)
+        a.ly[l].dres = ly[l].residual ? a.ly[l].dy : nullptr;
+        a.ly[l].poll_res = l < L - 1;
+        res = res || (ly[l].residual && ly[l].Wt);
     }
     a.flags = sync + XCD_FLAGS;
     a.timeout = timeout;
@@ -1187,6 +1348,10 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H * (L + nx),
                  (double)L * (sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0) +
                      nx * ((double)sh.T * sh.B * (G4 * 2.0 + sh.H * 2.0) + G4 * sh.H * 2.0));
+    if (res) {
+        if (sh.B <= 16) return launch256<lstm_bwd_wave<32, 1, true>>(s, &a);
+        return launch256<lstm_bwd_wave<32, 2, true>>(s, &a);
+    }
     if (sh.B <= 16) return launch256<lstm_bwd_wave<32, 1>>(s, &a);
     return launch256<lstm_bwd_wave<32, 2>>(s, &a);
 }

@@ -58,8 +58,8 @@ def load_library():
         "lstm_forward": ([H] + [vp] * 11 + [sz, vp, sz, vp], i),
         "lstm_backward": ([H] + [vp] * 11 + [sz] + [vp] * 7 + [i, vp, sz, vp], i),
         "lstm_forward_noalloc": ([H] + [vp] * 11 + [sz, vp], i),
-        "lstm_forward_stack": ([i] + [vp] * 7 + [sz, vp, sz, vp], i),
-        "lstm_backward_stack": ([i] + [vp] * 7 + [sz] + [vp] * 4 + [i, vp, sz, vp], i),
+        "lstm_forward_stack": ([i] + [vp] * 9 + [sz, vp, sz, vp], i),
+        "lstm_backward_stack": ([i] + [vp] * 9 + [sz] + [vp] * 4 + [i, vp, sz, vp], i),
         "lstm_backward_stack_workspace_size": ([i, vp], sz),
         "lstm_check": ([H, vp, vp], i),
         "lstm_destroy": ([H], i),
@@ -153,13 +153,23 @@ def lstm_forward_noalloc(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, stream=No
            "lstm_forward_noalloc")
 
 
-def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=None) -> bool:
+def _residual_args(n, residual, sums):
+    if not residual or not any(residual):
+        return None, None
+    flags = (ctypes.c_int * n)(*[int(bool(r)) for r in residual])
+    return flags, (ctypes.c_void_p * n)(*[_ptr(v) for v in sums])
+
+
+def lstm_forward_stack(handles, x, Ws, Rs, bs, ys, reserves, workspace, stream=None, residual=None,
+                       sums=None) -> bool:
     """Layer-wavefront forward of a stack (lstm_forward_stack).  Returns False,
     having computed nothing that counts, when the stack does not fit it
-    (LSTM_ERR_UNSUPPORTED); raises on any other error."""
+    (LSTM_ERR_UNSUPPORTED); raises on any other error.  residual[l] / sums[l]:
+    layer l's output is y_l plus its input, stored in sums[l]."""
     n = len(handles)
     arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
-    st = load_library().lstm_forward_stack(n, arr(handles), _ptr(x), arr(Ws), arr(Rs), arr(bs), arr(ys),
+    rf, sp = _residual_args(n, residual, sums)
+    st = load_library().lstm_forward_stack(n, arr(handles), _ptr(x), arr(Ws), arr(Rs), arr(bs), arr(ys), rf, sp,
                                            arr(reserves), min(_nbytes(r) for r in reserves), _ptr(workspace),
                                            _nbytes(workspace), _stream(stream))
     if st == LSTM_ERR_UNSUPPORTED:
@@ -174,13 +184,14 @@ def lstm_backward_stack_workspace_size(handles) -> int:
 
 
 def lstm_backward_stack(handles, dy, x, Ws, Rs, ys, reserves, dx, dWs, dRs, dbs, accumulate, workspace,
-                        stream=None) -> bool:
+                        stream=None, residual=None, sums=None) -> bool:
     """Layer-wavefront backward of a stack (lstm_backward_stack).  Returns
     False when the stack does not fit it (LSTM_ERR_UNSUPPORTED); raises on
     any other error."""
     n = len(handles)
     arr = lambda vals: (ctypes.c_void_p * n)(*[_ptr(v) for v in vals])
-    st = load_library().lstm_backward_stack(n, arr(handles), _ptr(dy), _ptr(x), arr(Ws), arr(Rs), arr(ys),
+    rf, sp = _residual_args(n, residual, sums)
+    st = load_library().lstm_backward_stack(n, arr(handles), _ptr(dy), _ptr(x), arr(Ws), arr(Rs), arr(ys), rf, sp,
                                             arr(reserves), min(_nbytes(r) for r in reserves), _ptr(dx), arr(dWs),
                                             arr(dRs), arr(dbs), int(bool(accumulate)), _ptr(workspace),
                                             _nbytes(workspace), _stream(stream))
@@ -364,18 +375,22 @@ class Stack:
         return grads
 
     def forward(self, x, params, stream=None):
-        # a stack of plain unidirectional layers runs as one layer wavefront
-        # when the library supports its shape (lstm_forward_stack)
+        # a stack of unidirectional LSTM layers (residual ones included) runs
+        # as one layer wavefront when the library supports its shape
+        # (lstm_forward_stack)
         self.last_forward = "layers"
         if (self.wavefront and 2 <= len(self.layers) <= 4 and self.dtype == "bf16"
-                and all(not L.bidirectional and not L.residual and not L.Hp for L in self.layers)):
+                and all(not L.bidirectional and not L.Hp for L in self.layers)):
             lays = [d[0] for d in self.dirs]
+            residual = [L.residual for L in self.layers]
             if lstm_forward_stack([l.handle for l in lays], x, [p[0]["W"] for p in params],
                                   [p[0]["R"] for p in params], [p[0]["b"] for p in params], self.y,
-                                  [l.reserve for l in lays], self.workspace, stream):
-                self.inputs = [x] + self.y[:-1]
+                                  [l.reserve for l in lays], self.workspace, stream, residual=residual,
+                                  sums=self.xout):
+                outs = [self.xout[li] if L.residual else self.y[li] for li, L in enumerate(self.layers)]
+                self.inputs = [x] + outs[:-1]
                 self.last_forward = "wavefront"
-                return self.y[-1]
+                return outs[-1]
         cur = x
         for li, L in enumerate(self.layers):
             self.inputs[li] = cur
@@ -407,7 +422,8 @@ class Stack:
                 if lstm_backward_stack(hs, d_out, self.inputs[0], [p[0]["W"] for p in params],
                                        [p[0]["R"] for p in params], self.y, [l.reserve for l in lays], dx,
                                        [g[0]["dW"] for g in grads], [g[0]["dR"] for g in grads],
-                                       [g[0]["db"] for g in grads], accumulate, self.wave_ws, stream):
+                                       [g[0]["db"] for g in grads], accumulate, self.wave_ws, stream,
+                                       residual=[L.residual for L in self.layers], sums=self.xout):
                     self.last_backward = "wavefront"
                     return dx
         g = d_out

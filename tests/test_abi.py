@@ -134,7 +134,8 @@ def test_forward_stack_validates_before_launch(lib):
 
     def call(hs, x=A, n=None, rb=BIG, wb=BIG):
         n = len(hs) if n is None else n
-        return lib.lstm_forward_stack(n, arr(hs), x, ptrs(n), ptrs(n), ptrs(n), ptrs(n), ptrs(n), rb, A, wb, None)
+        return lib.lstm_forward_stack(n, arr(hs), x, ptrs(n), ptrs(n), ptrs(n), ptrs(n), None, None, ptrs(n), rb, A, wb,
+                                      None)
 
     assert call(hb[:2], x=None) == L.LSTM_ERR_INVALID_ARG                  # missing input
     assert call(hb[:2], x=A + 2) == L.LSTM_ERR_INVALID_ARG                 # misaligned input
@@ -174,7 +175,7 @@ def test_backward_stack_validates_before_launch(lib):
     def call(hs, dy=A, acc=0, rb=BIG, wb=BIG):
         n = len(hs)
         p = arr([A] * n)
-        return lib.lstm_backward_stack(n, arr(hs), dy, A, p, p, p, p, rb, None, p, p, p, acc, A, wb, None)
+        return lib.lstm_backward_stack(n, arr(hs), dy, A, p, p, p, None, None, p, rb, None, p, p, p, acc, A, wb, None)
 
     assert call(hb, dy=None) == L.LSTM_ERR_INVALID_ARG
     assert call(hb, acc=2) == L.LSTM_ERR_INVALID_ARG

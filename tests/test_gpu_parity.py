@@ -380,6 +380,59 @@ def test_layer_wavefront_stack_parity(T, B, I0, nl):
     compare(gpu, ref, "bf16", label=wl.name)
 
 
+WAVE_RESIDUAL_CASES = [
+    # (T, B, residual flag of each layer)
+    (6, 16, (0, 0, 1, 1)),   # residual from the third layer on, as in the GNMT encoder
+    (5, 13, (0, 1, 1)),      # the sum formed in the launch feeds the top layer's sum
+    (4, 20, (1, 1)),         # the first layer adds the stack's input; two row blocks, ragged
+    (5, 32, (1, 0, 1)),      # a sum of the stack's input inside, the top sum after the launch
+    (3, 7, (0, 1, 0, 1)),
+    (6, 16, (1, 1, 1, 1)),   # every layer residual: each sum adds the one formed below it
+]
+
+
+@pytest.mark.parametrize("T,B,residual", WAVE_RESIDUAL_CASES)
+def test_layer_wavefront_residual_stack_parity(T, B, residual):
+    """Residual layers (output = y + input) in the layer wavefront: a layer's
+    projection forms its residual input from two exchanged row sets and
+    stores it, the top layer's sum follows the launch, and the backward's
+    input-gradient roles add each residual layer's upstream gradient (the
+    identity path).  Outputs and every gradient match the oracle."""
+    layers = [synth.LayerSpec(1024, 1024, residual=bool(r)) for r in residual]
+    wl = synth.Workload(f"wave_res_T{T}_B{B}_{''.join(map(str, residual))}", T=T, B=B, layers=layers,
+                        dtype="bf16", seed=31 + T + B, w_scale=0.05)
+    announce(f"layer wavefront, residual {residual}, T={T} B={B}")
+    prob = synth.draw(wl)
+    gpu, stack = run_stack_gpu(prob)
+    assert stack.last_forward == "wavefront" and stack.last_backward == "wavefront"
+    ref = run_oracle(prob)
+    compare(gpu, ref, "bf16", label=wl.name)
+
+
+def test_layer_wavefront_residual_matches_layer_by_layer():
+    """A residual stack through the wavefront and layer by layer (lstm_add for
+    the sums): the same outputs up to the summation order of the input
+    projection, and the same gradients up to it and to one rounding of the
+    input gradient (the wavefront adds the identity path before rounding)."""
+    from paper_1907_13257_amd import Stack
+    from _gpu_helpers import device_params, stack_layers
+    wl = synth.Workload("wave_res_vs_layers", T=8, B=16,
+                        layers=[synth.LayerSpec(1024, 1024, residual=r) for r in (False, True, True)],
+                        dtype="bf16", seed=41, w_scale=0.05)
+    announce("layer wavefront vs layers, residual")
+    prob = synth.draw(wl)
+    params = device_params(prob)
+    a, sa = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype), params=params)
+    b, sb = run_stack_gpu(prob, stack=Stack(wl.T, wl.B, stack_layers(wl), wl.dtype, wavefront=False), params=params)
+    assert sa.last_forward == "wavefront" and sb.last_forward == "layers"
+    assert sa.last_backward == "wavefront" and sb.last_backward == "layers"
+    assert normwise(a["y"], b["y"]) < 1e-2
+    assert normwise(a["dx"], b["dx"]) < 2e-2
+    for la, lb in zip(a["layers"], b["layers"]):
+        for k in ("dW", "dR", "db"):
+            assert normwise(la[0][k], lb[0][k]) < 2e-2, k
+
+
 def test_layer_wavefront_matches_layer_by_layer():
     """The wavefront and the layer-by-layer forward give the same outputs up
     to the summation order of the input projection."""
