@@ -371,6 +371,25 @@ __device__ __forceinline__ void read_frags(u32x4 (&f)[F], const char *base, int 
     }
 }
 
+// Four consecutive values of a row of C: one 16-byte fp32 store, or one
+// 8-byte store of four 16-bit values.
+template <typename TO>
+__device__ __forceinline__ void store4(TO *p, f32x4 v);
+template <>
+__device__ __forceinline__ void store4<float>(float *p, f32x4 v)
+{
+    *reinterpret_cast<f32x4 *>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t *p, f32x4 v)
+{
+    const unsigned lo = (unsigned)f32_to_bf16(v[0]) | ((unsigned)f32_to_bf16(v[1]) << 16);
+    const unsigned hi = (unsigned)f32_to_bf16(v[2]) | ((unsigned)f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<u32x2 *>(p) = u32x2{lo, hi};
+}
+
+__device__ __forceinline__ void wait_lds_only() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // Tile order: bands of g.band tile columns, each band row-major.  The XCD
 // groups take consecutive ranges of this order, so a group's tiles cover a
 // roughly square block of C and share both operands' rows in its L2 (the
@@ -604,6 +623,47 @@ void gemm_dl_kernel(GemmArgs g)
             g.cell_m[(long)row * g.cell_ldm + cell] = f32_to_bf16(og * tanh_f(c));
             if (g.cell_cT) g.cell_cT[e] = c;
         }
+        run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
+        return;
+    }
+    // Plain stores (no split, no accumulation into C, four-column aligned C):
+    // each 32x32 block goes through the wave's own LDS scratch so that every
+    // lane stores four consecutive columns of a row at once (16 bytes fp32, 8
+    // bytes 16-bit) instead of one element per block row: a quarter of the
+    // store instructions, which bound the epilogue more than its bytes do.
+    constexpr int SP = 36;                        // scratch row pitch (floats): 16-byte rows, few bank conflicts
+    static_assert(NW * 32 * SP * 4 <= NS * STAGE, "the epilogue scratch fits in the operand stages");
+    const bool vec_out = !split && !g.beta && (g.N % 4) == 0 && (ldc % 4) == 0 && (coff % 4) == 0 &&
+                         (reinterpret_cast<uintptr_t>(cbase) & (4 * sizeof(TO) - 1)) == 0;
+    if (vec_out) {
+        float *scr = reinterpret_cast<float *>(smem) + wave * 32 * SP;
+        __syncthreads();   // every wave has finished reading the operand stages
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                // lane holds column lane % 32 of rows 8 (v / 4) + 4 (lane / 32) + v % 4
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    scr[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * SP + (lane & 31)] = acc[i][j][v];
+                wait_lds_only();
+                // read back row-major: four consecutive columns per lane and pass
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int q = r * 64 + lane, rr = q >> 3, c4 = (q & 7) * 4;
+                    const f32x4 x4 = *reinterpret_cast<const f32x4 *>(&scr[rr * SP + c4]);
+                    const int row = m0 + wm * WM + i * 32 + rr, col = n0 + wn * WN + j * 32 + c4;
+                    if (row < g.M && col < g.N) {
+                        f32x4 o = x4;
+                        if (g.bias) {
+                            const f32x4 b4 = *reinterpret_cast<const f32x4 *>(&g.bias[col]);
+                            o = o + b4;
+                        }
+                        store4<TO>(cbase + (long)row * ldc + (col - coff), o);
+                    }
+                }
+                wait_lds_only();   // the reads are done before the next block overwrites the scratch
+            }
         run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
         return;
     }
