@@ -148,6 +148,18 @@ def test_forward_stack_validates_before_launch(lib):
     assert call(hb[:5]) == L.LSTM_ERR_UNSUPPORTED                          # five layers
     assert call(hf) == L.LSTM_ERR_UNSUPPORTED                              # fp32
     assert "wavefront" in L.lstm_last_error_detail()
+    # residual layers: a flag without its sum buffer, or on a layer whose input is narrower
+    flags = (ctypes.c_int * 2)(0, 1)
+    none2 = arr([None, None])
+    assert lib.lstm_forward_stack(2, arr(hb[:2]), A, ptrs(2), ptrs(2), ptrs(2), ptrs(2), flags, none2, ptrs(2),
+                                  BIG, A, BIG, None) == L.LSTM_ERR_INVALID_ARG
+    assert "sum" in L.lstm_last_error_detail()
+    hn = L.lstm_create(4, 8, 512, 1024, 0, "bf16")
+    flags0 = (ctypes.c_int * 2)(1, 0)
+    assert lib.lstm_forward_stack(2, arr([hn, hb[0]]), A, ptrs(2), ptrs(2), ptrs(2), ptrs(2), flags0, ptrs(2),
+                                  ptrs(2), BIG, A, BIG, None) == L.LSTM_ERR_INVALID_ARG
+    assert "wide" in L.lstm_last_error_detail()
+    L.lstm_destroy(hn)
     hr = L.lstm_create(4, 8, 1024, 1024, 0, "bf16", reverse=True)
     assert call([hb[0], hr]) == L.LSTM_ERR_UNSUPPORTED                     # a reversed layer
     hw = L.lstm_create(4, 8, 512, 1024, 0, "bf16")
@@ -182,6 +194,10 @@ def test_backward_stack_validates_before_launch(lib):
     assert call(hb, dy=A + 2) == L.LSTM_ERR_INVALID_ARG
     assert call([hn, hb[0]]) == L.LSTM_ERR_UNSUPPORTED
     assert call([h1, h1]) == L.LSTM_ERR_UNSUPPORTED
+    flags = (ctypes.c_int * 3)(1, 0, 0)   # the first layer's sum feeds the second layer's weight gradients
+    p3 = arr([A] * 3)
+    assert lib.lstm_backward_stack(3, arr(hb), A, A, p3, p3, p3, flags, arr([None] * 3), p3, BIG, None, p3, p3, p3,
+                                   0, A, BIG, None) == L.LSTM_ERR_INVALID_ARG
     assert call(hb, rb=L.lstm_reserve_size(hb[0]) - 1) == L.LSTM_ERR_WORKSPACE
     assert call(hb, wb=size - 1) == L.LSTM_ERR_WORKSPACE
     assert "workspace" in L.lstm_last_error_detail()
