@@ -724,8 +724,6 @@ struct WaveBwdLayer {
     const bf16_t *dy;          // [T][B][H] upstream gradient (for l < L-1 written by XCD 2l+3)
     bf16_t *dx;                // [T][B][H] input gradient (dy of layer l-1, or the stack's dx)
     float *dbp;                // [4H] bias gradient of layer l
-    const bf16_t *dres;        // residual layer: its upstream gradient, added to dx (the identity path)
-    int poll_res;              // dres is written in the launch
 };
 
 struct XWaveBwdArgs {
@@ -733,6 +731,7 @@ struct XWaveBwdArgs {
     WaveBwdLayer ly[4];
     unsigned *flags;
     unsigned long long timeout;
+    int res_mask;   // bit l: layer l is residual, its dy also reaches its dx unchanged
 };
 
 template <int HN, int MBX, bool RES = false>
@@ -756,6 +755,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
     if (layer >= a.L) return;
     const WaveBwdLayer ly = a.ly[layer];
     if (xrole && !ly.Wt) return;
+    const bool lres = RES && ((a.res_mask >> layer) & 1);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, slot = blockIdx.x >> 3;
     const int H = a.H, B = a.B, T = a.T;
     const long G4 = 4L * H;
@@ -799,15 +799,17 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
                 if (s_bad) return;
                 const bool vr = has_cell && rb0 + cr < B;
                 // residual layer: its upstream gradient also reaches its input unchanged
+                // (written in the launch by the layer above, except for the top layer)
                 bf16_t g = 0;
-                if (RES && ly.dres) {
+                if (RES && lres) {
+                    const bool poll_res = layer < a.L - 1;
                     const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
-                        const_cast<bf16_t *>(ly.dres), (short)0, (int)((long)T * B * H * 2), 0x00020000);
+                        const_cast<bf16_t *>(ly.dy), (short)0, (int)((long)T * B * H * 2), 0x00020000);
                     const unsigned off = (unsigned)((((long)s * B + rb0 + crr) * H + cj) * 2);
                     if (vr)   // sc1 (16): the rows written in the launch are read past L1
-                        g = ly.poll_res ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 16)
-                                        : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 0);
-                    if (ly.poll_res) {
+                        g = poll_res ? (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 16)
+                                     : (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(rres, off, 0, 0);
+                    if (poll_res) {
                         const __amdgpu_buffer_rsrc_t rfl = rsrc(a.flags);
                         const unsigned long long t0 = wall_clock64();
                         while (__builtin_amdgcn_ballot_w64(vr && g == NOT_READY) != 0) {
@@ -830,7 +832,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_wave(XWaveBwdArgs a)
                     float v = 0.0f;
 #pragma unroll
                     for (int q = 0; q < 8; ++q) v += red[q][cr][cu];
-                    if (RES && ly.dres) v += to_f32(g);
+                    if (RES && lres) v += to_f32(g);
                     __builtin_amdgcn_raw_buffer_store_b16(ready_value(f32_to_bf16(v)), rdx,
                                                           (unsigned)((((long)s * B + rb0 + cr) * H + cj) * 2), 0, 16);
                 }
@@ -1327,8 +1329,7 @@ hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly
         a.ly[l].dbp = ly[l].dbp;
         // a residual layer's input gradient adds its upstream gradient, which
         // the layer above writes in the launch (the stack's own for the top layer)
-        a.ly[l].dres = ly[l].residual ? a.ly[l].dy : nullptr;
-        a.ly[l].poll_res = l < L - 1;
+        if (ly[l].residual) a.res_mask |= 1 << l;
         res = res || (ly[l].residual && ly[l].Wt);
     }
     a.flags = sync + XCD_FLAGS;
