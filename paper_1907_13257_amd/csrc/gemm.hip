@@ -626,15 +626,18 @@ void gemm_dl_kernel(GemmArgs g)
         run_side_job(g.side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
         return;
     }
-    // Plain stores (no split, no accumulation into C, four-column aligned C):
-    // each 32x32 block goes through the wave's own LDS scratch so that every
-    // lane stores four consecutive columns of a row at once (16 bytes fp32, 8
-    // bytes 16-bit) instead of one element per block row: a quarter of the
-    // store instructions, which bound the epilogue more than its bytes do.
+    // Plain stores (no accumulation into C, four-column aligned C) and split
+    // partials: each 32x32 block goes through the wave's own LDS scratch so
+    // that every lane stores four consecutive columns of a row at once (16
+    // bytes fp32, 8 bytes 16-bit) instead of one element per block row: a
+    // quarter of the store instructions, which bound the epilogue more than
+    // its bytes do.
     constexpr int SP = 36;                        // scratch row pitch (floats): 16-byte rows, few bank conflicts
     static_assert(NW * 32 * SP * 4 <= NS * STAGE, "the epilogue scratch fits in the operand stages");
-    const bool vec_out = !split && !g.beta && (g.N % 4) == 0 && (ldc % 4) == 0 && (coff % 4) == 0 &&
-                         (reinterpret_cast<uintptr_t>(cbase) & (4 * sizeof(TO) - 1)) == 0;
+    const bool vec_out =
+        split ? (g.N % 4) == 0 && (reinterpret_cast<uintptr_t>(part) & 15) == 0
+              : !g.beta && (g.N % 4) == 0 && (ldc % 4) == 0 && (coff % 4) == 0 &&
+                    (reinterpret_cast<uintptr_t>(cbase) & (4 * sizeof(TO) - 1)) == 0;
     if (vec_out) {
         float *scr = reinterpret_cast<float *>(smem) + wave * 32 * SP;
         __syncthreads();   // every wave has finished reading the operand stages
@@ -654,12 +657,16 @@ void gemm_dl_kernel(GemmArgs g)
                     const f32x4 x4 = *reinterpret_cast<const f32x4 *>(&scr[rr * SP + c4]);
                     const int row = m0 + wm * WM + i * 32 + rr, col = n0 + wn * WN + j * 32 + c4;
                     if (row < g.M && col < g.N) {
-                        f32x4 o = x4;
-                        if (g.bias) {
-                            const f32x4 b4 = *reinterpret_cast<const f32x4 *>(&g.bias[col]);
-                            o = o + b4;
+                        if (split) {
+                            store4<float>(part + (long)row * g.N + col, x4);
+                        } else {
+                            f32x4 o = x4;
+                            if (g.bias) {
+                                const f32x4 b4 = *reinterpret_cast<const f32x4 *>(&g.bias[col]);
+                                o = o + b4;
+                            }
+                            store4<TO>(cbase + (long)row * ldc + (col - coff), o);
                         }
-                        store4<TO>(cbase + (long)row * ldc + (col - coff), o);
                     }
                 }
                 wait_lds_only();   // the reads are done before the next block overwrites the scratch
@@ -811,6 +818,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     g.band = band_width(tiles_m, g.tiles_n, g.per_xcd, BM, BN);
     g.kchunk = ((d.K + splits - 1) / splits + KD - 1) / KD * KD;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
+    if (d.partials > 1 && splits != d.partials) return hipErrorInvalidValue;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
     g.N1 = d.N1;
     g.B2 = static_cast<const char *>(d.B2); g.ldb2 = d.ldb2; g.b2_bytes = d.b2_bytes;
@@ -842,7 +850,7 @@ hipError_t launch_gemm_dl(const GemmDesc &d, int splits, hipStream_t s)
     }
     hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits, g.nbatch), dim3(64 * NWM * NWN), LDS, s, g);
     e = hipGetLastError();
-    if (e != hipSuccess || splits == 1) return e;
+    if (e != hipSuccess || splits == 1 || d.partials > 1) return e;
     return launch_splitk_reduce<TO>(d, splits, s);
 }
 
@@ -865,6 +873,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     g.band = g.tiles_n;
     g.kchunk = ((d.K + splits - 1) / splits + KS - 1) / KS * KS;
     splits = (d.K + g.kchunk - 1) / g.kchunk;
+    if (d.partials > 1 && splits != d.partials) return hipErrorInvalidValue;
     g.partial = splits > 1 ? d.splitk_ws : nullptr;
     g.N1 = 0; g.B2 = g.B3 = nullptr; g.C2 = nullptr;
     g.side = d.side;
@@ -876,7 +885,7 @@ hipError_t launch_gemm(const GemmDesc &d, int splits, hipStream_t s)
     }
     hipLaunchKernelGGL(kern, dim3(g.per_xcd * 8, splits), dim3(256), LDS, s, g);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || splits == 1) return e;
+    if (e != hipSuccess || splits == 1 || d.partials > 1) return e;
     return launch_splitk_reduce<TO>(d, splits, s);
 }
 
@@ -1166,6 +1175,10 @@ hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
     }
     if (d.N1 > 0) return hipErrorInvalidValue;
     Choice c = choose(d, sizeof(TI));
+    if (d.partials > 1) {   // exactly the requested parts, all of them in the workspace
+        if (d.nbatch > 1 || fit_splits(d, d.partials) != d.partials) return hipErrorInvalidValue;
+        c.splits = d.partials;
+    }
     c.splits = fit_splits(d, c.splits);   // also bounds a tuning override
     if constexpr (sizeof(TI) == 4) {
         return launch_gemm<TI, TO, 128, 128, 64, AK, BKM>(d, c.splits, s);
@@ -1217,6 +1230,7 @@ bool gemm_cell_ok(const GemmDesc &d)
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
 {
     if (d.M <= 0 || d.N <= 0 || d.K <= 0) return hipSuccess;
+    if (d.partials > 1 && (d.N1 > 0 || d.cell_h > 0 || d.nbatch > 1 || !d.splitk_ws)) return hipErrorInvalidValue;
     const double es = (double)dsize(d.in);
     double flops, bytes;
     if (d.N1 > 0) {   // second column block over its own k range

@@ -104,6 +104,10 @@ struct GemmDesc {
     // along K.
     int nbatch = 1;
     const GemmDesc *batch = nullptr;
+    // Partials: the product split along K into exactly this many parts (> 1),
+    // each part's fp32 sum written to splitk_ws[part][M][N] and left for the
+    // caller to add up (no reduction runs; C, bias and beta are not used).
+    int partials = 0;
 };
 // Whether `gemm` can run the fused cell update for descriptor d.
 bool gemm_cell_ok(const GemmDesc &d);

@@ -131,8 +131,16 @@ hipError_t backward_stepwise(DType t, const RecShape &sh, const BwdBufs &b, cons
             g.A = dH + (long)tt * B * Hp * es; g.lda = Hp;
             g.B = w.P; g.ldb = H;
             g.C = b.dhn; g.ldc = H;
+            // bf16: two halves of k on twice the workgroups (a few batch rows
+            // and no split give one workgroup per two CUs), their fp32 sums
+            // added by the gate gradients
+            const bool halves = t == DType::BF16 && Hp % 128 == 0 && w.splitk_ws &&
+                                w.splitk_ws_floats >= 2 * (size_t)B * H;
+            if (halves) g.partials = 2;
             RET_IF(gemm(g, s, K_REC_BWD));
-            RET_IF(gates_backward(t, B, H, b.dhn, nullptr, 0, nullptr, nullptr, gates_t, c_t, cprev, b.dcn, dz_t, dc0,
+            const float *dm0 = halves ? w.splitk_ws : b.dhn;
+            const float *dm1 = halves ? w.splitk_ws + (size_t)B * H : nullptr;
+            RET_IF(gates_backward(t, B, H, dm0, nullptr, 0, dm1, nullptr, gates_t, c_t, cprev, b.dcn, dz_t, dc0,
                                   K_REC_BWD, s));
         } else {
             const bool first = st == T - 1;
