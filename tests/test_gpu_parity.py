@@ -232,6 +232,70 @@ def test_zero_weights_closed_form(dtype, H):
         assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
+STATE_CARRY_CASES = [
+    # (T1, T2, B, I, H, Hp, dtype, path)
+    (4, 5, 16, 64, 256, 0, "bf16", "xcd"),
+    (3, 4, 10, 40, 96, 0, "f32", "generic"),
+    (3, 3, 20, 48, 128, 64, "bf16", "stepwise"),
+]
+
+
+@pytest.mark.parametrize("T1,T2,B,I,H,Hp,dtype,path", STATE_CARRY_CASES)
+def test_state_carry(T1, T2, B, I, H, Hp, dtype, path, monkeypatch):
+    """A sequence cut in two on the GPU (no oracle): the forward of steps
+    [0, T1) gives hT, cT, which start the forward of [T1, T1 + T2); the
+    backward of the second part gives dh0, dc0, which enter the backward of
+    the first part as dhT, dcT.  Outputs and input gradients of each part
+    equal those of the whole sequence in one call, the weight gradients of
+    the whole are the sums over the parts, and the whole's dh0, dc0 are the
+    first part's.  The cut changes only how the products are tiled over
+    time, so the bound is a tenth of the oracle tolerance."""
+    if path == "stepwise":
+        monkeypatch.setenv("LSTM355_RECURRENCE", "stepwise")
+    T = T1 + T2
+    label = f"state carry {path} T{T1}+{T2} B{B} I{I} H{H} Hp{Hp} {dtype}"
+    announce(label)
+    full_c = layer_case(T, B, I, H, Hp, dtype, False, seed=T * 31 + B)
+    full = run_layer_gpu(full_c, T, B, I, H, Hp, dtype, False)
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        want = {"xcd": XCD_VARIANT, "stepwise": STEPWISE_VARIANT}.get(path)
+        if want is not None:
+            assert full["tiling"][3] == want, full["tiling"]
+        else:
+            assert full["tiling"][3] not in (XCD_VARIANT, STEPWISE_VARIANT), full["tiling"]
+
+    def part(lo, hi, h0, c0, dhT, dcT):
+        c = dict(full_c)
+        c["x"] = synth.Tensor(full_c["x"].f64[lo:hi], dtype)
+        c["dy"] = synth.Tensor(full_c["dy"].f64[lo:hi], dtype)
+        c["h0"], c["c0"], c["dhT"], c["dcT"] = h0, c0, dhT, dcT
+        return c
+
+    # forward of the first part alone: its backward needs the second part's dh0, dc0
+    first_fwd = run_layer_gpu(part(0, T1, full_c["h0"], full_c["c0"], None, None), T1, B, I, H, Hp, dtype, False)
+    h_mid = synth.Tensor(first_fwd["hT"], dtype)   # bf16 and fp32 values are exact in fp64
+    c_mid = first_fwd["cT"].astype(np.float32)
+    second = run_layer_gpu(part(T1, T, h_mid, c_mid, full_c["dhT"], full_c["dcT"]), T2, B, I, H, Hp, dtype, False)
+    first = run_layer_gpu(part(0, T1, full_c["h0"], full_c["c0"], synth.Tensor(second["dh0"], dtype),
+                               second["dc0"].astype(np.float32)), T1, B, I, H, Hp, dtype, False)
+    errs = {
+        "y": normwise(np.concatenate([first["y"], second["y"]]), full["y"]),
+        "hT": normwise(second["hT"], full["hT"]),
+        "cT": normwise(second["cT"], full["cT"]),
+        "dx": normwise(np.concatenate([first["dx"], second["dx"]]), full["dx"]),
+        "dh0": normwise(first["dh0"], full["dh0"]),
+        "dc0": normwise(first["dc0"], full["dc0"]),
+    }
+    for k in ("dW", "dR", "db", "dP"):
+        if k in full:
+            errs[k] = normwise(first[k] + second[k], full[k])
+    exact = [k for k in ("y", "hT", "cT", "dx", "dh0", "dc0") if errs[k] == 0.0]
+    announce(f"{label} " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()) + f"; bitwise equal: {exact}")
+    tol = TOL[dtype]
+    bad = {k: v for k, v in errs.items() if v > 0.1 * (tol["out"] if k in ("y", "hT", "cT") else tol["grad"])}
+    assert not bad, f"{label}: {bad}"
+
+
 @pytest.mark.parametrize("T,B,I,H,dtype,must_trip", [(20, 24, 32, 72, "f32", True),
                                                       (20, 64, 32, 256, "bf16", False)])
 def test_watchdog_gives_up_from_host_and_next_call_succeeds(T, B, I, H, dtype, must_trip, monkeypatch):
