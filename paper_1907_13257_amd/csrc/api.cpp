@@ -216,10 +216,12 @@ lstm_status_t check_forward_args(lstm_handle_t h, const void *x, const void *h0,
 
 // One layer's forward pass (arguments validated, plan made): the input
 // projection, then the recurrence.  `wv` is the workspace (sync words at
-// w_sync; the stepwise recurrence also uses the split-K partials at w_split).
+// w_sync; the stepwise recurrence also uses the split-K partials at w_split);
+// full_ws: it is the whole workspace, not the allocation-free entry point's
+// scratch, so the XCD-local forward may keep an fp16 input projection in it.
 lstm_status_t forward_impl(lstm_handle_t h, const void *x, const void *h0, const float *c0, const void *W,
                            const void *R, const float *b, const void *P, void *y, void *hT, float *cT,
-                           void *reserve, char *wv, hipStream_t s)
+                           void *reserve, char *wv, bool full_ws, hipStream_t s)
 {
     const lstm_desc_t &d = h->d;
     char *rv = static_cast<char *>(reserve);
@@ -243,6 +245,18 @@ lstm_status_t forward_impl(lstm_handle_t h, const void *x, const void *h0, const
     g.C = gates; g.ldc = h->G4;
     g.bias = b; g.beta = 0;
     if (xcd) g.side = xcd_prep_forward(sh, fb);   // the recurrence's exchange rows and flags
+    if (xcd && full_ws) {
+        // the XCD-local forward takes the input projection in fp16, half the
+        // bytes of the product's output and of the recurrence's reads, in the
+        // workspace's dz rows (the backward's, unused by the forward)
+        GemmDesc g16 = g;
+        g16.out_f32 = false; g16.out_f16 = true;
+        g16.C = wv + h->w_dz;
+        if (gemm_f16_ok(g16)) {
+            g = g16;
+            fb.gx16 = g16.C;
+        }
+    }
     TRY_HIP("input projection", gemm(g, s, K_GEMM_GX));
 
     if (!xcd && use_stepwise(h, h->fwd_ok)) {
@@ -302,7 +316,7 @@ extern "C" lstm_status_t lstm_forward(lstm_handle_t h, const void *x, const void
         if (workspace_bytes < h->w_total) return short_buffer("workspace", workspace_bytes, h->w_total);
         st = ensure_plan(h);
         if (st != LSTM_OK) return st;
-        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, static_cast<char *>(workspace),
+        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, static_cast<char *>(workspace), true,
                             static_cast<hipStream_t>(stream));
     } catch (...) {
         return invalid("exception");
@@ -333,7 +347,7 @@ extern "C" lstm_status_t lstm_forward_noalloc(lstm_handle_t h, const void *x, co
         char *wv = nullptr;
         st = scratch_address(&wv);
         if (st != LSTM_OK) return st;
-        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, wv, static_cast<hipStream_t>(stream));
+        return forward_impl(h, x, h0, c0, W, R, b, P, y, hT, cT, reserve, wv, false, static_cast<hipStream_t>(stream));
     } catch (...) {
         return invalid("exception");
     }

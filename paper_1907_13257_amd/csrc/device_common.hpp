@@ -22,9 +22,21 @@ __device__ __forceinline__ float to_f32(bf16_t v) { return __uint_as_float(((uns
 // one instruction (v_cvt_pk_bf16_f32, rounding per the default RNE mode).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
+// fp16 (binary16) storage of the forward's input projection (the gate
+// pre-activations x W^T + b): three more mantissa bits than bf16.  The
+// conversion rounds to nearest even and saturates at +-65504, where every
+// gate function is flat to fp32 precision; NaN stays a NaN.
+typedef _Float16 f16_t;
+__device__ __forceinline__ float to_f32(f16_t v) { return (float)v; }
+__device__ __forceinline__ f16_t f32_to_f16_sat(float f)
+{
+    return (f16_t)(f == f ? __builtin_fminf(__builtin_fmaxf(f, -65504.0f), 65504.0f) : f);
+}
+
 template <typename TI> __device__ __forceinline__ TI from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+template <> __device__ __forceinline__ f16_t from_f32<f16_t>(float v) { return f32_to_f16_sat(v); }
 
 // Gate non-linearities in fp32.  sigma(u) = 1/(1+e^-u); tanh(u) = 2 sigma(2u) - 1.
 // The reciprocal is the hardware's (v_rcp_f32, within 1 ulp) rather than an

@@ -388,6 +388,14 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t *p, f32x4 v)
     *reinterpret_cast<u32x2 *>(p) = u32x2{lo, hi};
 }
 
+template <>
+__device__ __forceinline__ void store4<f16_t>(f16_t *p, f32x4 v)
+{
+    typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+    *reinterpret_cast<f16x4 *>(p) =
+        f16x4{f32_to_f16_sat(v[0]), f32_to_f16_sat(v[1]), f32_to_f16_sat(v[2]), f32_to_f16_sat(v[3])};
+}
+
 __device__ __forceinline__ void wait_lds_only() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // Tile order: bands of g.band tile columns, each band row-major.  The XCD
@@ -1220,6 +1228,17 @@ bool gemm_dual_ok(const GemmDesc &d)
     return dl_ok(d, 128, 128, 1);
 }
 
+// fp16 C only where the product takes the 256x256 tile unsplit (the same
+// shapes on which choose() picks it: more than 1024 rows, at least 192 tiles).
+bool gemm_f16_ok(const GemmDesc &d)
+{
+    if (d.in != DType::BF16 || !d.a_kmajor || !d.b_kmajor || d.out_f32 || d.beta || d.N1 > 0 || d.cell_h > 0 ||
+        d.nbatch > 1 || d.partials > 0 || d.M <= 1024)
+        return false;
+    const long tiles = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
+    return tiles >= 192 && tile_fits(d, 22);
+}
+
 bool gemm_cell_ok(const GemmDesc &d)
 {
     if (d.cell_h <= 0 || d.in != DType::BF16 || !d.a_kmajor || !d.b_kmajor || !d.out_f32 || !d.beta) return false;
@@ -1254,6 +1273,10 @@ hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass)
     ProfScope ps(kclass, s, flops, bytes);
     g_kclass = kclass;
     if (d.cell_h > 0) return launch_gemm_dl<float, 128, 64, true, true, 64, 3, 2, 2, true, true>(d, 1, s);
+    if (d.out_f16) {
+        if (!gemm_f16_ok(d)) return hipErrorInvalidValue;
+        return launch_gemm_dl<f16_t, 256, 256, true, true, 64, 2, 4, 4>(d, 1, s);
+    }
     return d.in == DType::BF16 ? dispatch_layout<bf16_t>(d, s) : dispatch_layout<float>(d, s);
 }
 

@@ -108,9 +108,14 @@ struct GemmDesc {
     // each part's fp32 sum written to splitk_ws[part][M][N] and left for the
     // caller to add up (no reduction runs; C, bias and beta are not used).
     int partials = 0;
+    // fp16 C (bf16 operands, both k-contiguous, no accumulation into C): the
+    // forward's input projection on the tiles gemm_f16_ok accepts.
+    bool out_f16 = false;
 };
 // Whether `gemm` can run the fused cell update for descriptor d.
 bool gemm_cell_ok(const GemmDesc &d);
+// Whether `gemm` can run descriptor d with an fp16 C (out_f16).
+bool gemm_f16_ok(const GemmDesc &d);
 hipError_t gemm(const GemmDesc &d, hipStream_t s, int kclass);
 // Whether a descriptor with a second column block (N1 > 0) can run.
 bool gemm_dual_ok(const GemmDesc &d);
@@ -186,6 +191,10 @@ struct FwdBufs {
     void *hT;
     float *cT;
     unsigned *sync;
+    // Optional [T][B][4H] fp16 Gx (XCD-local forward only): the input
+    // projection is read from here instead of from gates, which then only
+    // receives the activated gates.
+    const void *gx16 = nullptr;
 };
 hipError_t launch_forward(DType t, const RecShape &sh, const RecTiling &tl, const FwdBufs &b, hipStream_t s);
 

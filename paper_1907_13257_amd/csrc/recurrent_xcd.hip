@@ -307,6 +307,7 @@ struct XFwdArgs {
     const bf16_t *R, *h0;
     const float *c0;
     float *gates, *cs;
+    const uint16_t *gx;   // fp16 input projection [T][B][4H] (its bit patterns), or NULL: it is in gates
     bf16_t *y, *hT;
     float *cT;
     unsigned *flags;
@@ -320,7 +321,7 @@ struct XFwdArgs {
 // (gate rows x batch rows), so each lane ends with the four gates of one
 // cell for one batch row: one 16-byte LDS store per block, and the gate math
 // reads each wave's partial sums of a cell with one 16-byte load.
-template <int HN, int MBX>
+template <int HN, int MBX, bool GX16 = false>
 __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 {
     constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
@@ -373,15 +374,22 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
     for (int s = 0; s < a.T; ++s) {
         const int t = a.reverse ? a.T - 1 - s : s;
         const bool last = s == a.T - 1;
-        // input projection of this step for the own cells (independent of h_{t-1})
-        float gx[MBX][4];
+        // input projection of this step for the own cells (independent of
+        // h_{t-1}), kept as loaded (fp32 or fp16 bits) until the gate math so
+        // that no wait for these loads lands before the exchange
+        unsigned gxu[MBX][4];
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
             const int b = row0 + mb * 16 + cr;
             const bool v = has_cell && b < rowend;
-            const float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+            const long e = ((long)t * B + b) * G4 + cj;
+            if constexpr (GX16) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) gx[mb][g] = v ? gp[g * H] : 0.0f;
+                for (int g = 0; g < 4; ++g) gxu[mb][g] = v ? (unsigned)a.gx[e + g * H] : 0u;
+            } else {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) gxu[mb][g] = v ? __float_as_uint(a.gates[e + g * H]) : 0u;
+            }
         }
 #pragma unroll
         for (int mb = 0; mb < MBX; ++mb) {
@@ -422,7 +430,19 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
             const int b = rb0 + cr;
             const int crr = has_cell ? cr : 0;
             if (ALL_LANES || (has_cell && b < rowend)) {
-                float z[4] = {gx[mb][0], gx[mb][1], gx[mb][2], gx[mb][3]};
+                float z[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    unsigned u = gxu[mb][g];
+                    if constexpr (GX16) {
+                        // the conversion stays here: hoisted next to its load it
+                        // would make that load's wait a full memory latency
+                        asm volatile("" : "+v"(u));
+                        z[g] = to_f32(__builtin_bit_cast(f16_t, (uint16_t)u));
+                    } else {
+                        z[g] = __uint_as_float(u);
+                    }
+                }
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const f32x4 p = *reinterpret_cast<const f32x4 *>(&red[q][crr][4 * cu]);
@@ -1413,6 +1433,7 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     a.R = static_cast<const bf16_t *>(bf.R);
     a.h0 = static_cast<const bf16_t *>(bf.h0);
     a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
+    a.gx = static_cast<const uint16_t *>(bf.gx16);
     a.y = static_cast<bf16_t *>(bf.y);
     a.hT = static_cast<bf16_t *>(bf.hT);
     a.cT = bf.cT;
@@ -1426,11 +1447,14 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
         if (e != hipSuccess) return e;
     }
     const double G4 = 4.0 * sh.H;
+    // per row and step: the input projection read (fp32 or fp16), the
+    // activations written (fp32), c and h written
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
-                 (double)sh.T * sh.B * (G4 * 8.0 + sh.H * 6.0) + G4 * sh.H * 2.0);
+                 (double)sh.T * sh.B * (G4 * (a.gx ? 6.0 : 8.0) + sh.H * 6.0) + G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
-#define FWD_CASE(HN_, M_) \
-    if (sh.H == 32 * HN_ && m == M_) return launch256<lstm_fwd_xcd<HN_, M_>>(s, &a);
+#define FWD_CASE(HN_, M_)                                                                            \
+    if (sh.H == 32 * HN_ && m == M_)                                                                 \
+        return a.gx ? launch256<lstm_fwd_xcd<HN_, M_, true>>(s, &a) : launch256<lstm_fwd_xcd<HN_, M_>>(s, &a);
     FWD_CASE(8, 1) FWD_CASE(8, 2) FWD_CASE(8, 4)
     FWD_CASE(16, 1) FWD_CASE(16, 2) FWD_CASE(16, 4)
     FWD_CASE(32, 1) FWD_CASE(32, 2) FWD_CASE(32, 4)

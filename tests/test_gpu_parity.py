@@ -127,7 +127,8 @@ LAYER_CASES = [
     (2, 1, 8, 1024, 0, "bf16", True),      # one row in all, full-width cells
     (3, 136, 64, 1024, 0, "bf16", False),  # full-width cells, 17 rows per XCD: two row blocks
     (3, 264, 64, 1024, 0, "bf16", True),   # full-width cells, 33 rows per XCD: four row blocks, reverse
-    (13, 250, 64, 1024, 0, "bf16", False), # input projection on 256x256 tiles (208 of them, ragged last row)
+    (13, 250, 64, 1024, 0, "bf16", False), # input projection on 256x256 tiles (208 of them, ragged last row), in fp16
+    (12, 256, 64, 1024, 0, "bf16", True),  # the same on exactly 192 tiles, reverse
     # [dW | dR] as one product (bf16, B a multiple of 32, I and I + H multiples of 128)
     (4, 32, 128, 256, 0, "bf16", False),   # with h0: the first step's segment comes from h0
     (3, 64, 128, 256, 0, "bf16", True),    # reverse: h0 pairs with the last time index
