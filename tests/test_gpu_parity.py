@@ -249,8 +249,13 @@ def test_state_carry(T1, T2, B, I, H, Hp, dtype, path, monkeypatch):
     the first part as dhT, dcT.  Outputs and input gradients of each part
     equal those of the whole sequence in one call, the weight gradients of
     the whole are the sums over the parts, and the whole's dh0, dc0 are the
-    first part's.  The cut changes only how the products are tiled over
-    time, so the bound is a tenth of the oracle tolerance."""
+    first part's.  The forward carries h and c in their storage types (bf16
+    y, fp32 c) either way, and the cut changes only how the products are
+    tiled over time, so outputs are held to a tenth of the oracle tolerance
+    (they come out bitwise equal).  In bf16 mode the carried gradient dh is
+    rounded once to bf16 at the cut (dh0 and dhT are bf16 tensors), which the
+    whole sequence never does; one rounding unit is 2^-9 ~ 2e-3, and the
+    gradients are held to five of them (1e-2).  fp32 gradients: 1e-5."""
     if path == "stepwise":
         monkeypatch.setenv("LSTM355_RECURRENCE", "stepwise")
     T = T1 + T2
@@ -292,8 +297,9 @@ def test_state_carry(T1, T2, B, I, H, Hp, dtype, path, monkeypatch):
             errs[k] = normwise(first[k] + second[k], full[k])
     exact = [k for k in ("y", "hT", "cT", "dx", "dh0", "dc0") if errs[k] == 0.0]
     announce(f"{label} " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()) + f"; bitwise equal: {exact}")
-    tol = TOL[dtype]
-    bad = {k: v for k, v in errs.items() if v > 0.1 * (tol["out"] if k in ("y", "hT", "cT") else tol["grad"])}
+    out_tol = 0.1 * TOL[dtype]["out"]
+    grad_tol = 1e-2 if dtype == "bf16" else 1e-5
+    bad = {k: v for k, v in errs.items() if v > (out_tol if k in ("y", "hT", "cT") else grad_tol)}
     assert not bad, f"{label}: {bad}"
 
 
