@@ -22,7 +22,7 @@ struct lstm_handle {
     long ldx, ldy;
     long TB, G4;
     // reserve layout (bytes)
-    size_t r_gates, r_cs, r_ms, r_total;
+    size_t r_gates, r_cs, r_ms, r_act16, r_total;   // r_act16: 0 when the layer has no fp16 activations region
     // workspace layout (bytes)
     size_t w_sync, w_dz, w_rt, w_pt, w_dH, w_dcn, w_dhn, w_part, w_split, w_total;
     size_t split_floats;
@@ -156,6 +156,12 @@ extern "C" lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out
         h->r_gates = o; o = align256(o + (size_t)TB * G4 * 4);
         h->r_cs = o;    o = align256(o + (size_t)TB * d.H * 4);
         h->r_ms = o;    o = align256(o + (d.Hp ? (size_t)TB * d.H * h->es : 0));
+        {   // the fp16 activated gates of the XCD-local kernels, for the layers they keep them in fp16
+            const RecShape sh{d.T, d.B, d.I, d.H, d.Hp, d.reverse, ldy};
+            const bool act16 = xcd_act16(h->dt, sh);
+            h->r_act16 = act16 ? o : 0;
+            o = align256(o + (act16 ? (size_t)TB * G4 * 2 : 0));
+        }
         h->r_total = o;
         o = 0;
         h->w_sync = o; o = align256(o + SYNC_BYTES);
@@ -236,6 +242,7 @@ lstm_status_t forward_impl(lstm_handle_t h, const void *x, const void *h0, const
     fb.y = y; fb.hT = hT; fb.cT = cT;
     fb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
     const bool xcd = xcd_path_ok(h->dt, sh, h->num_cus);
+    if (xcd && h->r_act16) fb.act16 = rv + h->r_act16;
 
     GemmDesc g{};
     g.in = h->dt; g.out_f32 = true; g.a_kmajor = true; g.b_kmajor = true;
@@ -666,6 +673,7 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         BwdBufs bb{};
         bb.Rt = Rt; bb.Pt = Pt; bb.dy = dy; bb.dhT = dhT; bb.dcT = dcT; bb.h0 = h0; bb.c0 = c0;
         bb.gates = reinterpret_cast<const float *>(rv + h->r_gates);
+        bb.act16 = (xcd && h->r_act16) ? rv + h->r_act16 : nullptr;
         bb.cs = reinterpret_cast<const float *>(rv + h->r_cs);
         bb.dz = dz; bb.dH = dH;
         bb.dcn = reinterpret_cast<float *>(wv + h->w_dcn);

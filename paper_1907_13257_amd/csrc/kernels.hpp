@@ -192,9 +192,11 @@ struct FwdBufs {
     float *cT;
     unsigned *sync;
     // Optional [T][B][4H] fp16 Gx (XCD-local forward only): the input
-    // projection is read from here instead of from gates, which then only
-    // receives the activated gates.
+    // projection is read from here instead of from gates.
     const void *gx16 = nullptr;
+    // Optional [T][B][4H] fp16 activated gates saved for the backward
+    // (XCD-local forward only, xcd_act16 layers), instead of fp32 into gates.
+    void *act16 = nullptr;
 };
 hipError_t launch_forward(DType t, const RecShape &sh, const RecTiling &tl, const FwdBufs &b, hipStream_t s);
 
@@ -207,6 +209,7 @@ struct BwdBufs {
     const void *h0;
     const float *c0;
     const float *gates, *cs;
+    const void *act16;  // XCD-local backward of an xcd_act16 layer: the forward's fp16 activated gates
     void *dz;           // [T][B][4H]
     void *dH;           // [T][B][Hp] (LSTMP)
     float *dcn;         // [B][H] carry of dc between steps
@@ -289,6 +292,12 @@ FillRanges backward_wave_fills(const RecShape &sh, int L, const WaveBwdBufs *ly,
 hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
                                 unsigned long long timeout, hipStream_t s, bool prefilled = false);
 SideJob xcd_prep_forward(const RecShape &sh, const FwdBufs &b);
+// Whether the XCD-local kernels of a layer of this shape save the activated
+// gates in fp16 (in their own reserve region) rather than fp32 into gates:
+// layers with 5 to 32 batch rows per XCD, which the layer wavefront (at most
+// 4 rows per XCD) never takes.  A fixed property of the layer, so that the
+// forward and the backward agree on it.
+bool xcd_act16(DType t, const RecShape &sh);
 SideJob xcd_prep_backward(const RecShape &sh, const BwdBufs &b);
 hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &b, unsigned long long timeout, hipStream_t s,
                               bool prepared = false);

@@ -23,6 +23,7 @@
 // wave exits.
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "device_common.hpp"
 #include "kernels.hpp"
@@ -308,6 +309,7 @@ struct XFwdArgs {
     const float *c0;
     float *gates, *cs;
     const uint16_t *gx;   // fp16 input projection [T][B][4H] (its bit patterns), or NULL: it is in gates
+    f16_t *act;           // fp16 activated gates [T][B][4H] (ACT16), else they go to gates in fp32
     bf16_t *y, *hT;
     float *cT;
     unsigned *flags;
@@ -321,7 +323,7 @@ struct XFwdArgs {
 // (gate rows x batch rows), so each lane ends with the four gates of one
 // cell for one batch row: one 16-byte LDS store per block, and the gate math
 // reads each wave's partial sums of a cell with one 16-byte load.
-template <int HN, int MBX, bool GX16 = false>
+template <int HN, int MBX, bool GX16 = false, bool ACT16 = false>
 __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
 {
     constexpr int NT = 4 * HN;        // gate rows owned (i, f, g, o of HN cells)
@@ -458,11 +460,19 @@ __global__ __launch_bounds__(XT) void lstm_fwd_xcd(XFwdArgs a)
                     a.y[((long)t * B + b) * a.ldy + cj] = hv;
                     if (last && a.hT) a.hT[(long)b * H + cj] = hv;
                     // saved activations for the backward pass (not on the critical path)
-                    float *gp = a.gates + ((long)t * B + b) * G4 + cj;
-                    gp[0] = ig;
-                    gp[H] = fg;
-                    gp[2 * H] = gg;
-                    gp[3 * H] = og;
+                    if constexpr (ACT16) {
+                        f16_t *ap = a.act + ((long)t * B + b) * G4 + cj;
+                        ap[0] = (f16_t)ig;
+                        ap[H] = (f16_t)fg;
+                        ap[2 * H] = (f16_t)gg;
+                        ap[3 * H] = (f16_t)og;
+                    } else {
+                        float *gp = a.gates + ((long)t * B + b) * G4 + cj;
+                        gp[0] = ig;
+                        gp[H] = fg;
+                        gp[2 * H] = gg;
+                        gp[3 * H] = og;
+                    }
                     a.cs[((long)t * B + b) * H + cj] = c;
                     if (last && a.cT) a.cT[(long)b * H + cj] = c;
                 }
@@ -983,6 +993,7 @@ struct XBwdArgs {
     long ldy;
     const bf16_t *Rt, *dy, *dhT;
     const float *dcT, *c0, *gates, *cs;
+    const uint16_t *act;   // fp16 activated gates [T][B][4H] (ACT16), else they are in gates
     bf16_t *dz, *dh0;
     float *dc0;
     float *dbpart;          // [8][4H]: per-XCD sums over its rows and all steps of dz
@@ -991,18 +1002,32 @@ struct XBwdArgs {
 };
 
 // Per-cell inputs of one BPTT step (saved forward state and upstream gradient).
-// dy stays in its storage bits until it is used: converting it where it is
-// loaded would make the wave wait for that load, and with it for the dz
-// stores issued before it, ahead of the exchange copy.
-template <int MBX>
+// dy and fp16 activations stay in their storage bits until they are used:
+// converting them where they are loaded would make the wave wait for those
+// loads, and with them for the dz stores issued before, ahead of the
+// exchange copy.
+template <int MBX, bool ACT16>
 struct BwdIn {
     bf16_t dy[MBX];
-    float g[MBX][4], c[MBX], cp[MBX];
+    typename std::conditional<ACT16, unsigned, float>::type g[MBX][4];   // fp16 bit patterns or fp32
+    float c[MBX], cp[MBX];
 };
+
+// Four fp16 activations from their bit patterns, converted where they are
+// used (the empty asm keeps the conversion from moving up to the load).
+__device__ __forceinline__ void act_f32(const unsigned (&bits)[4], float (&v)[4])
+{
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        unsigned u = bits[g];
+        asm volatile("" : "+v"(u));
+        v[g] = to_f32(__builtin_bit_cast(f16_t, (uint16_t)u));
+    }
+}
 
 // Wave w multiplies the k range [w*H/2, (w+1)*H/2) of dh_{t-1} = R^T dz_t
 // (k over the 4H gate rows); the eight partial sums meet in LDS.
-template <int HN, int MBX>
+template <int HN, int MBX, bool ACT16 = false>
 __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 {
     constexpr int NBB = HN >= 16 ? HN / 16 : 1;   // 16-column blocks of owned cells
@@ -1038,7 +1063,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
 
     const bool has_cell = tid < NCELL;
     const int cr = tid / HN, cu = tid % HN, cj = j0 + cu;
-    auto load_inputs = [&](int s, BwdIn<MBX> &in) {
+    auto load_inputs = [&](int s, BwdIn<MBX, ACT16> &in) {
         const int t = a.reverse ? a.T - 1 - s : s;
         const int tp = a.reverse ? t + 1 : t - 1;
 #pragma unroll
@@ -1048,7 +1073,12 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             const long rt = (long)t * B + (v ? b : 0);
             in.dy[mb] = v ? a.dy[rt * a.ldy + cj] : (bf16_t)0;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) in.g[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
+            for (int g = 0; g < 4; ++g) {
+                if constexpr (ACT16)
+                    in.g[mb][g] = v ? (unsigned)a.act[rt * G4 + g * H + cj] : 0u;
+                else
+                    in.g[mb][g] = v ? a.gates[rt * G4 + g * H + cj] : 0.0f;
+            }
             in.c[mb] = v ? a.cs[rt * H + cj] : 0.0f;
             in.cp[mb] = (v && s > 0) ? a.cs[((long)tp * B + b) * H + cj]
                                      : ((v && a.c0) ? a.c0[(long)(v ? b : 0) * H + cj] : 0.0f);
@@ -1064,7 +1094,7 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
         dhn[mb] = (v && a.dhT) ? to_f32(a.dhT[(long)b * H + cj]) : 0.0f;
         dcn[mb] = (v && a.dcT) ? a.dcT[(long)b * H + cj] : 0.0f;
     }
-    BwdIn<MBX> in;
+    BwdIn<MBX, ACT16> in;
     load_inputs(a.T - 1, in);
     __shared__ int s_bad;
     if (tid == 0) s_bad = 0;   // ordered by the first barrier below
@@ -1083,7 +1113,14 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             const int b = row0 + mb * 16 + cr;
             const bool v = has_cell && b < rowend;
             if (!ALL_LANES && !v) continue;
-            const float ig = in.g[mb][0], fg = in.g[mb][1], gg = in.g[mb][2], og = in.g[mb][3];
+            float gv[4];
+            if constexpr (ACT16) {
+                act_f32(in.g[mb], gv);
+            } else {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) gv[g] = in.g[mb][g];
+            }
+            const float ig = gv[0], fg = gv[1], gg = gv[2], og = gv[3];
             const float dm = to_f32(in.dy[mb]) + dhn[mb];
             const float tc = tanh_f(in.c[mb]);
             const float d_o = dm * tc;
@@ -1204,6 +1241,13 @@ hipError_t launch256(hipStream_t s, void *argp)
 int g_xcd_disabled = 0;
 
 }  // namespace
+
+bool xcd_act16(DType t, const RecShape &sh)
+{
+    if (t != DType::BF16 || sh.Hp != 0 || (sh.H != 256 && sh.H != 512 && sh.H != 1024)) return false;
+    const int RX = (sh.B + NXCD - 1) / NXCD;
+    return RX >= 5 && RX <= 32;
+}
 
 bool xcd_path_ok(DType t, const RecShape &sh, int num_cus)
 {
@@ -1434,6 +1478,7 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     a.h0 = static_cast<const bf16_t *>(bf.h0);
     a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
     a.gx = static_cast<const uint16_t *>(bf.gx16);
+    a.act = static_cast<f16_t *>(bf.act16);
     a.y = static_cast<bf16_t *>(bf.y);
     a.hT = static_cast<bf16_t *>(bf.hT);
     a.cT = bf.cT;
@@ -1448,17 +1493,30 @@ hipError_t launch_forward_xcd(const RecShape &sh, const FwdBufs &bf, unsigned lo
     }
     const double G4 = 4.0 * sh.H;
     // per row and step: the input projection read (fp32 or fp16), the
-    // activations written (fp32), c and h written
+    // activations written (fp32 or fp16), c and h written
     ProfScope ps(K_REC_FWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
-                 (double)sh.T * sh.B * (G4 * (a.gx ? 6.0 : 8.0) + sh.H * 6.0) + G4 * sh.H * 2.0);
+                 (double)sh.T * sh.B * (G4 * ((a.gx ? 2.0 : 4.0) + (a.act ? 2.0 : 4.0)) + sh.H * 6.0) +
+                     G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
-#define FWD_CASE(HN_, M_)                                                                            \
-    if (sh.H == 32 * HN_ && m == M_)                                                                 \
+    if ((a.act != nullptr) != xcd_act16(DType::BF16, sh)) return hipErrorInvalidValue;
+#define FWD_CASE(HN_, M_)                                                                   \
+    if (sh.H == 32 * HN_ && m == M_)                                                        \
         return a.gx ? launch256<lstm_fwd_xcd<HN_, M_, true>>(s, &a) : launch256<lstm_fwd_xcd<HN_, M_>>(s, &a);
+#define FWD_CASE_ACT(HN_, M_)                                                                         \
+    if (sh.H == 32 * HN_ && m == M_)                                                                  \
+        return a.gx ? launch256<lstm_fwd_xcd<HN_, M_, true, true>>(s, &a)                             \
+                    : launch256<lstm_fwd_xcd<HN_, M_, false, true>>(s, &a);
+    if (a.act) {
+        FWD_CASE_ACT(8, 1) FWD_CASE_ACT(8, 2)
+        FWD_CASE_ACT(16, 1) FWD_CASE_ACT(16, 2)
+        FWD_CASE_ACT(32, 1) FWD_CASE_ACT(32, 2)
+        return hipErrorInvalidValue;
+    }
     FWD_CASE(8, 1) FWD_CASE(8, 2) FWD_CASE(8, 4)
     FWD_CASE(16, 1) FWD_CASE(16, 2) FWD_CASE(16, 4)
     FWD_CASE(32, 1) FWD_CASE(32, 2) FWD_CASE(32, 4)
 #undef FWD_CASE
+#undef FWD_CASE_ACT
     return hipErrorInvalidValue;
 }
 
@@ -1471,6 +1529,7 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
     a.dy = static_cast<const bf16_t *>(bf.dy);
     a.dhT = static_cast<const bf16_t *>(bf.dhT);
     a.dcT = bf.dcT; a.c0 = bf.c0; a.gates = bf.gates; a.cs = bf.cs;
+    a.act = static_cast<const uint16_t *>(bf.act16);
     a.dz = static_cast<bf16_t *>(bf.dz);
     a.dh0 = static_cast<bf16_t *>(bf.dh0);
     a.dc0 = bf.dc0;
@@ -1485,15 +1544,26 @@ hipError_t launch_backward_xcd(const RecShape &sh, const BwdBufs &bf, unsigned l
         if (e != hipSuccess) return e;
     }
     const double G4 = 4.0 * sh.H;
+    // per row and step: the activations (fp32 or fp16), c and dy read, dz written
     ProfScope ps(K_REC_BWD, s, 2.0 * sh.T * sh.B * G4 * sh.H,
-                 (double)sh.T * sh.B * (G4 * 4.0 + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0);
+                 (double)sh.T * sh.B * (G4 * (a.act ? 2.0 : 4.0) + sh.H * 6.0 + G4 * 2.0) + G4 * sh.H * 2.0);
     const int m = mbx_for(sh.B);
+    if ((a.act != nullptr) != xcd_act16(DType::BF16, sh)) return hipErrorInvalidValue;
 #define BWD_CASE(HN_, M_) \
     if (sh.H == 32 * HN_ && m == M_) return launch256<lstm_bwd_xcd<HN_, M_>>(s, &a);
+#define BWD_CASE_ACT(HN_, M_) \
+    if (sh.H == 32 * HN_ && m == M_) return launch256<lstm_bwd_xcd<HN_, M_, true>>(s, &a);
+    if (a.act) {
+        BWD_CASE_ACT(8, 1) BWD_CASE_ACT(8, 2)
+        BWD_CASE_ACT(16, 1) BWD_CASE_ACT(16, 2)
+        BWD_CASE_ACT(32, 1) BWD_CASE_ACT(32, 2)
+        return hipErrorInvalidValue;
+    }
     BWD_CASE(8, 1) BWD_CASE(8, 2) BWD_CASE(8, 4)
     BWD_CASE(16, 1) BWD_CASE(16, 2) BWD_CASE(16, 4)
     BWD_CASE(32, 1) BWD_CASE(32, 2) BWD_CASE(32, 4)
 #undef BWD_CASE
+#undef BWD_CASE_ACT
     return hipErrorInvalidValue;
 }
 
