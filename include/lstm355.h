@@ -58,7 +58,9 @@ typedef enum {
 
 typedef enum {
     LSTM_F32 = 0,   /* fp32 storage and fp32 matrix-core arithmetic */
-    LSTM_BF16 = 1   /* bf16 storage; fp32 accumulation, gates and cell state */
+    LSTM_BF16 = 1   /* bf16 storage; fp32 accumulation, gates and cell state (the
+                       XCD-local kernels keep the input projection, and for 33 to
+                       256 batch rows the saved activated gates, in fp16) */
 } lstm_dtype_t;
 
 typedef struct {
@@ -74,8 +76,12 @@ typedef struct {
 lstm_status_t lstm_create(const lstm_desc_t *desc, lstm_handle_t *out);
 
 /* Bytes of `reserve`: written by lstm_forward, read by lstm_backward.  Holds
- * the activated gates [T][B][4H] and cell states [T][B][H] (fp32), and for
- * LSTMP the pre-projection outputs m[T][B][H]. */
+ * the activated gates [T][B][4H] and cell states [T][B][H] (fp32), for LSTMP
+ * the pre-projection outputs m[T][B][H], and for the layers whose XCD-local
+ * kernels save the activated gates in fp16 (bf16, plain LSTM, H in {256, 512,
+ * 1024}, 33 to 256 batch rows) a further [T][B][4H] fp16 region.  Its
+ * contents are the library's own, valid only for lstm_backward on the same
+ * handle and device. */
 size_t lstm_reserve_size(lstm_handle_t h);
 
 /* Bytes of `workspace` (scratch for one call at a time: barrier counters,
