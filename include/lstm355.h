@@ -58,9 +58,11 @@ typedef enum {
 
 typedef enum {
     LSTM_F32 = 0,   /* fp32 storage and fp32 matrix-core arithmetic */
-    LSTM_BF16 = 1   /* bf16 storage; fp32 accumulation, gates and cell state (the
-                       XCD-local kernels keep the input projection, and for 33 to
-                       256 batch rows the saved activated gates, in fp16) */
+    LSTM_BF16 = 1   /* bf16 storage; fp32 accumulation, gates and cell state.  The
+                       XCD-local kernels store two intermediates in fp16: the input
+                       projection in lstm_forward when it spans more than 1024 rows
+                       T*B and at least 192 tiles of 256x256, and the saved
+                       activated gates for 33 to 256 batch rows. */
 } lstm_dtype_t;
 
 typedef struct {
