@@ -517,6 +517,38 @@ void gemm_dl_kernel(GemmArgs g)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
+    // Fused cell update: the C tile (the input projection, read through the
+    // cell-major column remap) and the previous cell state do not depend on
+    // the product, so they are loaded before the main loop and their latency
+    // overlaps it.  The loads are older than stage 0's, so the first stage
+    // wait covers them too.
+    constexpr int CELLS_T = BN / 4;
+    constexpr int NQ = GT ? (BM * CELLS_T) / (64 * NW) : 1;   // (row, cell) pairs per thread
+    static_assert(!GT || NQ * 64 * NW == BM * CELLS_T, "the cell pairs split evenly over the threads");
+    float cpre[GT ? FM : 1][GT ? FN : 1][16];
+    float cprev_pre[NQ];
+    if constexpr (GT) {
+        const float *cg = reinterpret_cast<const float *>(g.C);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int col = n0 + wn * WN + j * 32 + (lane & 31);
+                const long cc = (long)(col & 3) * g.cell_h + (col >> 2);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                    cpre[i][j][v] = (row < g.M && col < g.N) ? cg[(long)row * g.ldc + cc] : 0.0f;
+                }
+            }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int p = tid + q * 64 * NW, row = m0 + p / CELLS_T, cell = n0 / 4 + p % CELLS_T;
+            cprev_pre[q] = (g.cell_prev && row < g.M && cell < g.cell_h) ? g.cell_prev[(long)row * g.cell_h + cell]
+                                                                         : 0.0f;
+        }
+    }
+
     const unsigned sbase = lds_addr(smem);
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
@@ -571,7 +603,14 @@ void gemm_dl_kernel(GemmArgs g)
     // other instantiations add C element by element: the staging registers
     // would lower their occupancy.
     constexpr bool CPRE = CB;
-    if (CPRE && !split && g.beta) {
+    if constexpr (GT) {   // C was loaded before the main loop
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] += cpre[i][j][v];
+    } else if (CPRE && !split && g.beta) {
         constexpr int CJ = 1;   // one 32x32 block (16 values) per batch of loads
 #pragma unroll
         for (int i = 0; i < FM; ++i)
@@ -611,17 +650,17 @@ void gemm_dl_kernel(GemmArgs g)
                     zt[r * ZP + wn * WN + j * 32 + (lane & 31)] = acc[i][j][v];
                 }
         __syncthreads();
-        constexpr int CELLS = BN / 4;
         const int H = g.cell_h;
-        for (int p = tid; p < BM * CELLS; p += 64 * NW) {
-            const int r = p / CELLS, u = p % CELLS;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int p = tid + q * 64 * NW;
+            const int r = p / CELLS_T, u = p % CELLS_T;
             const int row = m0 + r, cell = n0 / 4 + u;
             if (row >= g.M || cell >= H) continue;
             const f32x4 z = *reinterpret_cast<const f32x4 *>(&zt[r * ZP + 4 * u]);
             const float ig = sigmoid_f(z[0]), fg = sigmoid_f(z[1]), gg = tanh_f(z[2]), og = sigmoid_f(z[3]);
             const long e = (long)row * H + cell;
-            const float cp = g.cell_prev ? g.cell_prev[e] : 0.0f;
-            const float c = fg * cp + ig * gg;
+            const float c = fg * cprev_pre[q] + ig * gg;
             float *gp = reinterpret_cast<float *>(cbase) + (long)row * ldc + cell;
             gp[0] = ig;
             gp[H] = fg;
