@@ -233,6 +233,30 @@ def test_zero_weights_closed_form(dtype, H):
         assert (gpu["tiling"][3] == XCD_VARIANT) == xcd, gpu["tiling"]
 
 
+def test_fp16_projection_saturates():
+    """The XCD-local forward's fp16 input projection (more than 1024 rows T*B,
+    at least 192 tiles of 256x256) saturates at +-65504.  With the bias scaled
+    by 1e6 (b ~ U(+-1e5), exact in fp32 and added in the product's epilogue,
+    so no large partial sums) a third of the pre-activations lie beyond
+    that; every gate function is flat to fp32 precision there, so the outputs
+    still match the oracle, which carries the exact values.  Gradients
+    through saturated gates vanish and are not compared."""
+    T, B, I, H = 12, 256, 1024, 1024
+    label = f"fp16 projection saturation T{T} B{B} I{I} H{H}"
+    announce(label)
+    c = layer_case(T, B, I, H, 0, "bf16", False, seed=4242, scale=0.1)
+    c["b"] = (c["b"].astype(np.float64) * 1.0e6).astype(np.float32)
+    assert np.mean(np.abs(c["b"]) > 65504.0) > 0.3   # the case exercises the saturation
+    gpu = run_layer_gpu(c, T, B, I, H, 0, "bf16", False)
+    ref = oracle.layer_forward(f64(c["x"]), f64(c["W"]), f64(c["R"]), f64(c["b"]), None, f64(c["h0"]),
+                               f64(c["c0"]), reverse=False)
+    errs = {k: normwise(gpu[k], ref[k]) for k in ("y", "hT", "cT")}
+    announce(f"{label} tiling={gpu['tiling']} " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert gpu["tiling"][3] == XCD_VARIANT, gpu["tiling"]
+    assert max(errs.values()) <= TOL["bf16"]["out"], errs
+
+
 STATE_CARRY_CASES = [
     # (T1, T2, B, I, H, Hp, dtype, path)
     (4, 5, 16, 64, 256, 0, "bf16", "xcd"),
