@@ -109,6 +109,11 @@ __device__ __forceinline__ u32x4 buffer_desc(const void *base, long bytes)
 
 __device__ __forceinline__ unsigned lds_addr(const void *p) { return (unsigned)(uintptr_t)p; }
 
+// M0 is a register the compiler reserves; naming it as clobbered draws a
+// warning but still orders the compiler's own M0 loads around the asm (the
+// generated code differs without it), so it stays and the warning is off here.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(u32x4 rsrc, unsigned lds_byte, unsigned voff)
 {
     asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
@@ -127,6 +132,7 @@ __device__ __forceinline__ void dma16_sc1(u32x4 rsrc, unsigned lds_byte, unsigne
                  : "s"(lds_byte), "v"(voff), "s"(rsrc)
                  : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 // s_waitcnt vmcnt(N) with expcnt and lgkmcnt not waited on (gfx9 encoding:
 // vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).

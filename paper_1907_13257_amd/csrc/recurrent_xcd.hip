@@ -700,7 +700,6 @@ __global__ __launch_bounds__(XT) void lstm_fwd_wave(XWaveArgs a)
                         s_bad = 1;
                         break;
                     }
-#pragma unroll
                     for (int g = 0; g < 4; ++g)
                         if (vrow && gxu[mb][g] == NOT_READY_F32)
                             gxu[mb][g] = __builtin_amdgcn_raw_buffer_load_b32(rg, goff + (unsigned)(g * H * 4), 0, 16);
