@@ -1040,6 +1040,19 @@ Choice choose(const GemmDesc &d, size_t es)
         return Choice{18, model_splits(d, 64, 128, kTileSlots[18], kTileKD[18])};
     }
     const double cu_rate = 4096.0 * 2.4e9 * 0.7;   // FLOP/s of one CU at a realistic fraction
+    if (es == 2 && d.a_kmajor && d.K >= 16384 && tile_fits(d, 22)) {
+        // a very long K over few output tiles (BigLSTM's dX, K = 4H = 32768):
+        // 256x256 tiles split along K to about one workgroup per CU.  Measured
+        // at 2560 x 1024 x 32768: 243 us with 128x128 tiles as the model splits
+        // them, 193 us on 256x128 split 3 ways, 170 us on 256x256 split 6 ways
+        const long tiles = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
+        if (tiles <= 128) {
+            int sp = (int)(256 / tiles);
+            if (sp > 8) sp = 8;
+            while (sp > 1 && d.K / sp < 2048) --sp;
+            return Choice{22, sp};
+        }
+    }
     if (es == 2 && d.a_kmajor && d.b_kmajor && tile_fits(d, 22)) {
         // both operands k-contiguous (the input projection) with enough
         // 256x256 tiles to occupy most CUs: one 16-wave workgroup per CU
