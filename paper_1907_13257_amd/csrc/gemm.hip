@@ -1053,6 +1053,14 @@ Choice choose(const GemmDesc &d, size_t es)
             return Choice{22, sp};
         }
     }
+    if (es == 2 && d.a_kmajor && !d.b_kmajor && tile_fits(d, 22)) {
+        // dX = dZ W: 256x256 tiles of 16 waves once they occupy three quarters
+        // of the CUs.  Measured: GNMT-4 B = 256 (200 tiles) 142 -> 107 us,
+        // B = 512 269 -> 216 us, GNMT-8 155 -> 119 us; at B = 128 (100 tiles)
+        // they lose (65.6 -> 71.2 us)
+        const long tiles = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
+        if (tiles >= 192) return Choice{22, 1};
+    }
     if (es == 2 && d.a_kmajor && d.b_kmajor && tile_fits(d, 22)) {
         // both operands k-contiguous (the input projection) with enough
         // 256x256 tiles to occupy most CUs: one 16-wave workgroup per CU
@@ -1073,8 +1081,11 @@ Choice choose(const GemmDesc &d, size_t es)
     }
     if (es == 2 && dl_ok(d, 128, 128, 1)) {
         // direct-to-LDS 128x128 tiles run two workgroups per CU (512 slots);
-        // split K only to fill the slots
-        Choice best{3, 1};
+        // split K only to fill the slots.  dX's layout takes 64-deep stages in
+        // a ring of two (B = 128 65.6 -> 64.1 us, B = 64 44.8 -> 42.7 us), the
+        // other products 32-deep stages in a ring of four
+        const int t128 = (d.a_kmajor && !d.b_kmajor && tile_fits(d, 5)) ? 5 : 3;
+        Choice best{t128, 1};
         double best_t = 1e30;
         const long tiles = (long)((d.M + 127) / 128) * ((d.N + 127) / 128);
         for (int sp = 1; sp <= 64; sp *= 2) {   // skinny products (per-step recurrences) split K widely
@@ -1086,7 +1097,7 @@ Choice choose(const GemmDesc &d, size_t es)
             if (sp > 1) tt += ((double)sp + 1.0) * d.M * d.N * 4.0 / 5.0e12;
             if (tt < best_t * 0.97) {
                 best_t = tt;
-                best = Choice{3, sp};
+                best = Choice{t128, sp};
             }
         }
         return best;
