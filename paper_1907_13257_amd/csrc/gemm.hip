@@ -1237,10 +1237,13 @@ hipError_t dispatch_tiles(const GemmDesc &d, hipStream_t s)
     if constexpr (sizeof(TI) == 2 && !AK && !BKM) {
         if (d.N1 > 0) {   // two column blocks: no split; 128x128 tiles, 64-deep stages where they fit
             Choice c{5, 1};
-            // 256x256 tiles of 16 waves once they fill the CUs at least once
-            // (BigLSTM's 32768 x 2048 product: 368 -> 324 us; at 4096 rows their
-            // 128 tiles leave half the CUs idle)
-            if ((long)(d.M / 256) * (d.N / 256) >= 256 && tile_fits(d, 22)) c.tile = 22;
+            // 256x256 tiles of 16 waves once the launch's tiles fill the CUs at
+            // least once (BigLSTM's 32768 x 2048 product: 368 -> 324 us; the
+            // layer wavefront's four 4096 x 2048 products in one launch: 73.7 ->
+            // 69.8 us at B = 16, 123.9 -> 109.7 us at B = 32; one 4096-row
+            // product's 128 tiles leave half the CUs idle)
+            const long nb = d.nbatch > 1 ? d.nbatch : 1;
+            if ((long)(d.M / 256) * (d.N / 256) * nb >= 256 && tile_fits(d, 22)) c.tile = 22;
             env_choice(&c);
             if (!tile_fits(d, c.tile)) c.tile = 5;
             if (!tile_fits(d, c.tile)) c.tile = 3;
