@@ -214,6 +214,130 @@ __device__ __forceinline__ bool stage_mma_when_ready(u32x4 rs, long r0, long ld,
     }
 }
 
+// Chunked staging: a wave's slice (16 rows x KCW 32-deep k chunks) is copied
+// in pairs of chunks, 64 k values = 128 bytes per row: pair p goes to LDS
+// block p (2 KiB, row i at byte 128*i), with two 1 KiB instructions of 8
+// whole rows each, so a wave can multiply the first pairs while the later
+// ones are still on their way.  Lane l of instruction h moves 16-byte piece
+// l % 8 of row 8h + l/8; within a row, piece P sits at slot P ^ ((row/2) % 8),
+// which puts the 16 rows that one fragment read touches in distinct banks.
+// Rows at or past `valid` are not copied (an offset past the descriptor's end
+// loads zeros).
+constexpr unsigned OOB_OFFSET = 0x80000000u;
+
+__device__ __forceinline__ unsigned pair_voff(long r0, long ld, int kbyte, int lane, int h, int valid)
+{
+    const int r = 8 * h + (lane >> 3), piece = (lane & 7) ^ ((r >> 1) & 7);
+    return r < valid ? (unsigned)((r0 + r) * ld * 2 + kbyte + piece * 16) : OOB_OFFSET;
+}
+
+__device__ __forceinline__ u32x4 pair_frag(const char *tilep, int c, int lane)
+{
+    const int i = lane & 15, piece = 4 * (c & 1) + (lane >> 4);
+    return *reinterpret_cast<const u32x4 *>(tilep + (c >> 1) * 2048 + i * 128 + ((piece ^ ((i >> 1) & 7)) * 16));
+}
+
+// s_waitcnt vmcnt(n), n in [0, 15]; n is a constant once the caller's loop
+// is unrolled, and the switch folds to the one instruction.
+__device__ __forceinline__ void wait_loads_upto(int n)
+{
+#define LSTM355_VMCNT(N)                                      \
+    case N:                                                   \
+        asm volatile("s_waitcnt vmcnt(" #N ")" ::: "memory"); \
+        break;
+    switch (n) {
+        LSTM355_VMCNT(0) LSTM355_VMCNT(1) LSTM355_VMCNT(2) LSTM355_VMCNT(3)
+        LSTM355_VMCNT(4) LSTM355_VMCNT(5) LSTM355_VMCNT(6) LSTM355_VMCNT(7)
+        LSTM355_VMCNT(8) LSTM355_VMCNT(9) LSTM355_VMCNT(10) LSTM355_VMCNT(11)
+        LSTM355_VMCNT(12) LSTM355_VMCNT(13) LSTM355_VMCNT(14)
+        default: asm volatile("s_waitcnt vmcnt(15)" ::: "memory"); break;
+    }
+#undef LSTM355_VMCNT
+}
+
+// The pipelined form of stage_mma_when_ready: all copies are issued at once
+// (two instructions per chunk pair, KCW in all); each group of G chunks is
+// multiplied as soon as its own copies have landed and none of its valid
+// elements holds NOT_READY.  A group that saw one is copied again together
+// with every later pair (they were copied at the same time, so they are
+// likely stale too), until it is complete.  Chunks are multiplied in order,
+// so the sums are those of the unpipelined form, bit for bit.
+template <int KCW, int NBX, bool WT, int G>
+__device__ __forceinline__ bool stage_mma_pipe(u32x4 rs, long r0, long ld, int kbyte, unsigned tile,
+                                               const char *tilep, int lane, int valid,
+                                               const u32x4 (&rf)[NBX][KCW], f32x4 (&acc)[NBX], unsigned *flags,
+                                               unsigned long long timeout)
+{
+    static_assert(KCW >= 2 && KCW <= 16 && KCW % 2 == 0, "whole chunk pairs, at most 16 instructions in flight");
+    static_assert(G % 2 == 0 && KCW % G == 0, "whole pairs per group, whole groups");
+    const unsigned v0 = pair_voff(r0, ld, kbyte, lane, 0, valid);
+    const unsigned v1 = pair_voff(r0, ld, kbyte, lane, 1, valid);
+    const bool row_in = (lane & 15) < valid;
+    auto issue_from = [&](int p0) {
+#pragma unroll
+        for (int p = 0; p < KCW / 2; ++p) {
+            if (p < p0) continue;
+            const unsigned blk = tile + p * 2048;
+            dma16_sc1(rs, __builtin_amdgcn_readfirstlane(blk), v0 + p * 128);
+            dma16_sc1(rs, __builtin_amdgcn_readfirstlane(blk + 1024), v1 + p * 128);
+        }
+    };
+    issue_from(0);
+#pragma unroll
+    for (int i = 0; i < NBX; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const __amdgpu_buffer_rsrc_t rfl = rsrc(flags);
+    unsigned long long t0 = 0;
+    bool waited = false;
+#pragma unroll
+    for (int c0 = 0; c0 < KCW; c0 += G) {
+        // the newest instructions are always the copies of pairs c0/2 .. KCW/2-1
+        wait_loads_upto(KCW - G - c0);
+        u32x4 fa[G];
+        u16x2 seen = {0, 0};
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            fa[g] = pair_frag(tilep, c0 + g, lane);
+            seen = max_halves(seen, fa[g]);
+        }
+        while (__builtin_amdgcn_ballot_w64(saw_not_ready(seen) && row_in) != 0) {
+            if (!waited) {
+                t0 = wall_clock64();
+                waited = true;
+            }
+            const unsigned ab = __builtin_amdgcn_raw_buffer_load_b32(rfl, XCD_ABORT * 4, 0, 16);
+            wait_own_loads();
+            if (ab != 0) return false;
+            if (wall_clock64() - t0 > timeout) {
+                if (lane == 0) {
+                    __hip_atomic_fetch_or(&g_xcd_tripped, TRIP_WATCHDOG, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(flags + XCD_ABORT, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                return false;
+            }
+            wait_own_lds();   // the fragments are in registers before their blocks are overwritten
+            issue_from(c0 / 2);
+            wait_loads_upto(KCW - G - c0);
+            seen = u16x2{0, 0};
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                fa[g] = pair_frag(tilep, c0 + g, lane);
+                seen = max_halves(seen, fa[g]);
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int i = 0; i < NBX; ++i) {
+                if (WT)
+                    mfma16(acc[i], rf[i][c0 + g], fa[g], bf16_t{});
+                else
+                    mfma16(acc[i], fa[g], rf[i][c0 + g], bf16_t{});
+            }
+    }
+    return true;
+}
+
 // a + b of eight bf16 pairs, in fp32, rounded to bf16 as the element-wise
 // add kernel rounds them (a result equal to NOT_READY becomes the canonical
 // NaN, as for every exchanged value).
@@ -1152,9 +1276,19 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             f32x4 acc[NBB];
 #pragma unroll
             for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if (!stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile, stage[w], lane,
-                                                    rowend - rb0, rf, acc, a.flags, a.timeout, slot))
-                s_bad = 1;
+            // With two or more row blocks the copy is pipelined in two halves
+            // (GNMT-4, B = 256: 336 -> 307 us per layer); with one, the first
+            // copy usually finds rows still missing, and re-copying just the
+            // missing rows after one full copy is faster (163 -> 170 us).
+            bool ok;
+            if constexpr (MBX >= 2)
+                ok = stage_mma_pipe<KCW, NBB, false, KCW / 2>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile,
+                                                              stage[w], lane, rowend - rb0, rf, acc, a.flags,
+                                                              a.timeout);
+            else
+                ok = stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile, stage[w],
+                                                        lane, rowend - rb0, rf, acc, a.flags, a.timeout, slot);
+            if (!ok) s_bad = 1;
 #pragma unroll
             for (int i = 0; i < NBB; ++i)
 #pragma unroll
