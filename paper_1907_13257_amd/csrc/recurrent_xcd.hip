@@ -338,6 +338,26 @@ __device__ __forceinline__ bool stage_mma_pipe(u32x4 rs, long r0, long ld, int k
     return true;
 }
 
+// The dz rows of a BPTT step times the resident R^T rows, for the per-layer
+// backward.  With two or more row blocks per XCD the copy is pipelined in two
+// halves (GNMT-4, B = 256: 336 -> 307 us per layer); with one, the first copy
+// usually finds rows still missing, and re-copying just the missing rows
+// after one full copy is faster (163 -> 170 us when pipelined).  The layer
+// wavefront's two row blocks (17 to 32 rows in one XCD) lose with it too
+// (B = 32: 355 -> 367 us), and keep the unpipelined copy.
+template <int RB, int KCW, int NBB, int MBX>
+__device__ __forceinline__ bool stage_dz(u32x4 rs, long r0, long ld, int kbyte, unsigned tile, const char *tilep,
+                                         int lane, int valid, const u32x4 (&rf)[NBB][KCW], f32x4 (&acc)[NBB],
+                                         unsigned *flags, unsigned long long timeout, int rot)
+{
+    if constexpr (MBX >= 2)
+        return stage_mma_pipe<KCW, NBB, false, KCW / 2>(rs, r0, ld, kbyte, tile, tilep, lane, valid, rf, acc, flags,
+                                                        timeout);
+    else
+        return stage_mma_when_ready<RB, KCW, NBB>(rs, r0, ld, kbyte, tile, tilep, lane, valid, rf, acc, flags,
+                                                  timeout, rot);
+}
+
 // a + b of eight bf16 pairs, in fp32, rounded to bf16 as the element-wise
 // add kernel rounds them (a result equal to NOT_READY becomes the canonical
 // NaN, as for every exchanged value).
@@ -1276,19 +1296,9 @@ __global__ __launch_bounds__(XT) void lstm_bwd_xcd(XBwdArgs a)
             f32x4 acc[NBB];
 #pragma unroll
             for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            // With two or more row blocks the copy is pipelined in two halves
-            // (GNMT-4, B = 256: 336 -> 307 us per layer); with one, the first
-            // copy usually finds rows still missing, and re-copying just the
-            // missing rows after one full copy is faster (163 -> 170 us).
-            bool ok;
-            if constexpr (MBX >= 2)
-                ok = stage_mma_pipe<KCW, NBB, false, KCW / 2>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile,
-                                                              stage[w], lane, rowend - rb0, rf, acc, a.flags,
-                                                              a.timeout);
-            else
-                ok = stage_mma_when_ready<RB, KCW, NBB>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile, stage[w],
-                                                        lane, rowend - rb0, rf, acc, a.flags, a.timeout, slot);
-            if (!ok) s_bad = 1;
+            if (!stage_dz<RB, KCW, NBB, MBX>(rs_dz, (long)t * B + rb0, G4, w * KW * 2, tile, stage[w], lane,
+                                             rowend - rb0, rf, acc, a.flags, a.timeout, slot))
+                s_bad = 1;
 #pragma unroll
             for (int i = 0; i < NBB; ++i)
 #pragma unroll
