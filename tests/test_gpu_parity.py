@@ -619,6 +619,24 @@ def test_deterministic():
                 assert np.array_equal(ga[k], gb[k]), k
 
 
+@pytest.mark.parametrize("B", [256, 264, 512])
+def test_deterministic_xcd_row_blocks(B):
+    """The XCD-local backward with two and four 16-row blocks per XCD (32, 33
+    and 64 rows) copies dz in pipelined halves and copies again whatever was
+    not yet written, so how many copies a step takes depends on timing; the
+    products still add the chunks in one fixed order, so two runs give
+    bitwise-identical outputs and gradients."""
+    T, I, H = 6, 1024, 1024
+    announce(f"determinism xcd T{T} B{B}")
+    c = layer_case(T, B, I, H, seed=B, scale=0.1)
+    a = run_layer_gpu(c, T, B, I, H, 0, "bf16", False)
+    b = run_layer_gpu(c, T, B, I, H, 0, "bf16", False)
+    rx = (B + 7) // 8
+    assert a["tiling"][3] == 1000 and a["tiling"][7] == 1000 and a["tiling"][6] == rx, a["tiling"]
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0", "dW", "dR", "db"):
+        assert np.array_equal(a[k], b[k]), k
+
+
 @pytest.mark.parametrize("dtype,n,off", [("bf16", 5040, 0), ("bf16", 1003, 0), ("bf16", 4096, 1), ("f32", 4099, 0),
                                          ("f32", 4096, 0)])
 def test_add_bitwise(dtype, n, off):
