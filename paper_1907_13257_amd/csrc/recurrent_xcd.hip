@@ -255,14 +255,14 @@ __device__ __forceinline__ void wait_loads_upto(int n)
 #undef LSTM355_VMCNT
 }
 
-// The pipelined form of stage_mma_when_ready: all copies are issued at once
-// (two instructions per chunk pair, KCW in all); each group of G chunks is
-// multiplied as soon as its own copies have landed and none of its valid
-// elements holds NOT_READY.  A group that saw one is copied again together
+// The pipelined form of stage_mma_when_ready (untransposed product): all
+// copies are issued at once (two instructions per chunk pair, KCW in all);
+// each group of G chunks is multiplied as soon as its own copies have landed
+// and none of its valid elements holds NOT_READY.  A group that saw one is copied again together
 // with every later pair (they were copied at the same time, so they are
 // likely stale too), until it is complete.  Chunks are multiplied in order,
 // so the sums are those of the unpipelined form, bit for bit.
-template <int KCW, int NBX, bool WT, int G>
+template <int KCW, int NBX, int G>
 __device__ __forceinline__ bool stage_mma_pipe(u32x4 rs, long r0, long ld, int kbyte, unsigned tile,
                                                const char *tilep, int lane, int valid,
                                                const u32x4 (&rf)[NBX][KCW], f32x4 (&acc)[NBX], unsigned *flags,
@@ -328,12 +328,7 @@ __device__ __forceinline__ bool stage_mma_pipe(u32x4 rs, long r0, long ld, int k
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int i = 0; i < NBX; ++i) {
-                if (WT)
-                    mfma16(acc[i], rf[i][c0 + g], fa[g], bf16_t{});
-                else
-                    mfma16(acc[i], fa[g], rf[i][c0 + g], bf16_t{});
-            }
+            for (int i = 0; i < NBX; ++i) mfma16(acc[i], fa[g], rf[i][c0 + g], bf16_t{});
     }
     return true;
 }
@@ -351,7 +346,7 @@ __device__ __forceinline__ bool stage_dz(u32x4 rs, long r0, long ld, int kbyte, 
                                          unsigned *flags, unsigned long long timeout, int rot)
 {
     if constexpr (MBX >= 2)
-        return stage_mma_pipe<KCW, NBB, false, KCW / 2>(rs, r0, ld, kbyte, tile, tilep, lane, valid, rf, acc, flags,
+        return stage_mma_pipe<KCW, NBB, KCW / 2>(rs, r0, ld, kbyte, tile, tilep, lane, valid, rf, acc, flags,
                                                         timeout);
     else
         return stage_mma_when_ready<RB, KCW, NBB>(rs, r0, ld, kbyte, tile, tilep, lane, valid, rf, acc, flags,
