@@ -194,9 +194,8 @@ lstm_status_t lstm_backward(lstm_handle_t h,
  *   dx: gradient of x [T][B][H], NULL when not wanted.
  *   dW[l], dR[l], db[l]: fp32 weight gradients of layer l; accumulate as for
  *     lstm_backward.
- *   workspace: lstm_backward_stack_workspace_size(L, h) bytes (per-layer R^T,
- *     W^T and dz, and the gradients passed between layers); workspace_bytes
- *     is its size.
+ *   workspace: lstm_backward_stack_workspace_size(L, h) bytes (per-layer dz
+ *     and the gradients passed between layers); workspace_bytes is its size.
  * Runs when L is 2..4, T >= 2, H = 1024 and B <= 32 on an MI355X whose
  * XCD-local path is enabled; otherwise returns LSTM_ERR_UNSUPPORTED and the
  * caller runs lstm_backward layer by layer. */

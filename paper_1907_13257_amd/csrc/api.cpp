@@ -463,11 +463,11 @@ extern "C" lstm_status_t lstm_forward_stack(int L, const lstm_handle_t *hs, cons
 }
 
 namespace {
-// Workspace of lstm_backward_stack: flags, then per layer R^T, W^T, dz and
-// (below the top layer) the upstream gradient written inside the launch,
-// then the bias gradients.
+// Workspace of lstm_backward_stack: flags, then per layer dz and (below the
+// top layer) the upstream gradient written inside the launch, then the bias
+// gradients.
 struct StackBwdLayout {
-    size_t sync, rt[4], wt[4], dz[4], dy[4], dbp, total;
+    size_t sync, dz[4], dy[4], dbp, total;
 };
 
 StackBwdLayout stack_bwd_layout(int L, const lstm_desc_t &d)
@@ -482,8 +482,6 @@ StackBwdLayout stack_bwd_layout(int L, const lstm_desc_t &d)
     const size_t H = (size_t)d.H, TB = (size_t)d.T * d.B;
     w.sync = take((size_t)(XCD_FLAGS + XCD_WORDS) * 4);
     for (int l = 0; l < L; ++l) {
-        w.rt[l] = take(4 * H * H * 2);
-        w.wt[l] = take(4 * H * H * 2);
         w.dz[l] = take(TB * 4 * H * 2);
         w.dy[l] = l < L - 1 ? take(TB * H * 2) : 0;
     }
@@ -592,18 +590,11 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
         }
         hipStream_t s = static_cast<hipStream_t>(stream);
         WaveBwdBufs wb[4];
-        const void *tsrc[8];
-        void *tdst[8];
-        int nt = 0;
-        for (int l = 0; l < L; ++l) {
-            tsrc[nt] = R[l]; tdst[nt++] = wv + lay.rt[l];
-            if (l > 0 || dx) { tsrc[nt] = W[l]; tdst[nt++] = wv + lay.wt[l]; }
-        }
         for (int l = 0; l < L; ++l) {
             const char *rv = static_cast<const char *>(reserve[l]);
             const bool want_dx = l > 0 || dx;
-            wb[l].Rt = wv + lay.rt[l];
-            wb[l].Wt = want_dx ? wv + lay.wt[l] : nullptr;
+            wb[l].R = R[l];
+            wb[l].W = want_dx ? W[l] : nullptr;
             wb[l].gates = reinterpret_cast<const float *>(rv + hs[l]->r_gates);
             wb[l].cs = reinterpret_cast<const float *>(rv + hs[l]->r_cs);
             wb[l].dz = wv + lay.dz[l];
@@ -613,13 +604,11 @@ extern "C" lstm_status_t lstm_backward_stack(int L, const lstm_handle_t *hs, con
             wb[l].dbp = reinterpret_cast<float *>(wv + lay.dbp) + (size_t)l * G4;
             wb[l].residual = res(l) ? 1 : 0;
         }
-        // one launch transposes R and W of every layer and arms the rows the
-        // wavefront exchanges; then the wavefront itself
+        // one launch arms the rows the wavefront exchanges, then the wavefront
+        // itself (its workgroups read the columns of R and W they keep)
         RecShape sh{T, B, H, H, 0, 0, hs[0]->ldy};
         unsigned *sync = reinterpret_cast<unsigned *>(wv + lay.sync);
-        const FillRanges fills = backward_wave_fills(sh, L, wb, sync);
-        TRY_HIP("transpose R, W", transpose_batch_u16(nt, tsrc, tdst, (int)G4, H, s, &fills));
-        TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, sync, watchdog_ticks(), s, true));
+        TRY_HIP("layer wavefront (backward)", launch_backward_wave(sh, L, wb, sync, watchdog_ticks(), s, false));
         // the layers' weight-gradient products as one batched launch
         GemmDesc gb = gw[0];
         gb.nbatch = L;
@@ -682,6 +671,8 @@ extern "C" lstm_status_t lstm_backward(lstm_handle_t h, const void *dy, const vo
         bb.dbpart = reinterpret_cast<float *>(wv + h->w_part);
         bb.sync = reinterpret_cast<unsigned *>(wv + h->w_sync);
         if (!stepwise) {   // the persistent kernels keep rows of R^T (and P^T)
+            // (reading R's columns in the kernel instead measured slower here:
+            // the transpose hides behind the exchange fill it carries)
             const SideJob prep = xcd ? xcd_prep_backward(sh, bb) : SideJob{};
             TRY_HIP("transpose R", transpose(h->dt, R, (int)G4, Hr, Rt, s, xcd ? &prep : nullptr));
             if (Hp) TRY_HIP("transpose P", transpose(h->dt, P, Hp, H, Pt, s));

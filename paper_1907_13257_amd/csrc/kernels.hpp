@@ -132,11 +132,6 @@ struct FillRanges {
     uint32_t v[FILL_MAX];
     int count;
 };
-// n (1..8) 16-bit matrices of one shape [rows][cols] (multiples of 64,
-// 16-byte aligned) transposed in one launch, which also performs `fill`
-// (if given) in slices of its own.
-hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s,
-                               const FillRanges *fill = nullptr);
 hipError_t fill_u32(void *p, size_t n, uint32_t v, hipStream_t s);
 // p[r*ld + c] = v for r < rows, c < cols (16-bit elements).
 hipError_t fill_rows_u16(void *p, long rows, int cols, long ld, uint16_t v, hipStream_t s);
@@ -276,7 +271,7 @@ hipError_t launch_forward_wave(const RecShape &sh, int L, const void *x, const W
 // layer, else the dx of the layer above, which this launch writes: dy_fill
 // is the same buffer, armed before the launch); dbp [4H] the bias gradient.
 struct WaveBwdBufs {
-    const void *Rt, *Wt;
+    const void *R, *W;   // R_l, W_l [4H][H] (W NULL: no input gradient wanted)
     const float *gates, *cs;
     void *dz;
     const void *dy;
@@ -287,7 +282,7 @@ struct WaveBwdBufs {
 };
 // The fills launch_backward_wave needs before its launch (flags, dz, the
 // upstream gradients written inside the launch); with `prefilled` the caller
-// has performed them (e.g. inside transpose_batch_u16).
+// has performed them.
 FillRanges backward_wave_fills(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync);
 hipError_t launch_backward_wave(const RecShape &sh, int L, const WaveBwdBufs *ly, unsigned *sync,
                                 unsigned long long timeout, hipStream_t s, bool prefilled = false);

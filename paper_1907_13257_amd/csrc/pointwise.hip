@@ -58,31 +58,6 @@ __global__ __launch_bounds__(256) void transpose_u16_vec_kernel(const uint16_t *
     run_side_job(side, (long)blockIdx.y * gridDim.x + blockIdx.x, (long)gridDim.x * gridDim.y);
 }
 
-// Several matrices of one shape in one launch: matrix blockIdx.z.
-struct TransposeBatch {
-    const uint16_t *src[8];
-    uint16_t *dst[8];
-};
-
-__global__ __launch_bounds__(256) void transpose_u16_vec_batch_kernel(TransposeBatch b, int n, int rows, int cols,
-                                                                      FillRanges f)
-{
-    if ((int)blockIdx.z < n) {
-        transpose_u16_vec_tile(b.src[blockIdx.z], rows, cols, b.dst[blockIdx.z]);
-        return;
-    }
-    // slice z - n: fill range z - n, 16-byte stores where the range allows them
-    const int r = blockIdx.z - n;
-    uint32_t *p = f.p[r];
-    const long cnt = f.n[r];
-    const uint32_t v = f.v[r];
-    const long wg = (long)blockIdx.y * gridDim.x + blockIdx.x, stride = (long)gridDim.x * gridDim.y * 256;
-    const bool vec = (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
-    const long nv = vec ? cnt / 4 : 0;
-    for (long i = wg * 256 + threadIdx.x; i < nv; i += stride) reinterpret_cast<u32x4 *>(p)[i] = u32x4{v, v, v, v};
-    for (long i = nv * 4 + wg * 256 + threadIdx.x; i < cnt; i += stride) p[i] = v;
-}
-
 __global__ void fill_kernel(uint32_t *p, size_t n, uint32_t v)
 {
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
@@ -368,27 +343,6 @@ hipError_t transpose(DType t, const void *src, int rows, int cols, void *dst, hi
     else
         hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, static_cast<const float *>(src), rows, cols,
                            static_cast<float *>(dst), sj);
-    return hipGetLastError();
-}
-
-hipError_t transpose_batch_u16(int n, const void *const *src, void *const *dst, int rows, int cols, hipStream_t s,
-                               const FillRanges *fill)
-{
-    if (n < 1 || n > 8 || rows % 64 || cols % 64) return hipErrorInvalidValue;
-    const FillRanges f = fill ? *fill : FillRanges{};
-    if (f.count < 0 || f.count > FILL_MAX) return hipErrorInvalidValue;
-    TransposeBatch b{};
-    for (int i = 0; i < n; ++i) {
-        if (((reinterpret_cast<uintptr_t>(src[i]) | reinterpret_cast<uintptr_t>(dst[i])) & 15) != 0)
-            return hipErrorInvalidValue;
-        b.src[i] = static_cast<const uint16_t *>(src[i]);
-        b.dst[i] = static_cast<uint16_t *>(dst[i]);
-    }
-    double bytes = 4.0 * n * (double)rows * cols;
-    for (int r = 0; r < f.count; ++r) bytes += 4.0 * f.n[r];
-    ProfScope ps(K_SMALL, s, 0.0, bytes);
-    hipLaunchKernelGGL(transpose_u16_vec_batch_kernel, dim3(cols / 64, rows / 64, n + f.count), dim3(256), 0, s, b, n,
-                       rows, cols, f);
     return hipGetLastError();
 }
 

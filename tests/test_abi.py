@@ -174,8 +174,10 @@ def test_backward_stack_validates_before_launch(lib):
     arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
     hb = [L.lstm_create(6, 8, 1024, 1024, 0, "bf16") for _ in range(3)]
     size = L.lstm_backward_stack_workspace_size(hb)
-    mat, tb = 4 * 1024 * 1024 * 2, 6 * 8
-    assert size >= 3 * (2 * mat + tb * 4096 * 2) + 2 * tb * 1024 * 2
+    tb = 6 * 8
+    # per layer dz, below the top layer the gradient passed down; the kernels
+    # read R and W themselves, so no transposed weights are kept
+    assert 3 * tb * 4096 * 2 + 2 * tb * 1024 * 2 <= size < 3 * 4 * 1024 * 1024 * 2
     assert L.lstm_backward_stack_workspace_size(hb[:1]) == 0          # one layer
     h1 = L.lstm_create(1, 8, 1024, 1024, 0, "bf16")
     assert L.lstm_backward_stack_workspace_size([h1, h1]) == 0         # T = 1
