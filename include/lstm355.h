@@ -25,9 +25,11 @@
  *     tensors (c0, cT, dcT, dc0), the bias and every weight gradient are fp32.
  *   - The caller owns every buffer.  The handle owns only its host-side
  *     descriptor and tiling choice.  Buffers must be 16-byte aligned.
- *   - Every call is asynchronous on `stream` (a hipStream_t) and returns a
- *     status; nothing throws or aborts across this boundary.  Arguments are
- *     validated on the host before anything is launched.
+ *   - Every call is asynchronous on `stream` (a hipStream_t, NULL for the
+ *     default stream, passed as void * so that this header needs no HIP
+ *     header) and returns a status; nothing throws or aborts across this
+ *     boundary.  Arguments are validated on the host before anything is
+ *     launched.
  *   - Calls on one handle that use the same workspace must be ordered (same
  *     stream); overlapping calls need distinct workspaces.
  *   - `reserve_bytes` / `workspace_bytes` give the sizes of the caller's
