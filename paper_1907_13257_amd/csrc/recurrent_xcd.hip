@@ -376,7 +376,6 @@ __device__ __forceinline__ void load_resident_cols(const bf16_t *M, long ld, lon
                                                    u32x4 (&rf)[HN >= 16 ? HN / 16 : 1][KW / 32])
 {
     constexpr int NBB = HN >= 16 ? HN / 16 : 1;
-    constexpr int KCW = KW / 32;
     constexpr int PITCH = 32 * NBB;           // bytes per staged k-row: NC = 16 NBB columns
     constexpr int PR = KW / NBB;              // k-rows per pass
     constexpr int RPI = 1024 / PITCH;         // k-rows per 1 KiB instruction
