@@ -33,6 +33,30 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 GEMM_CLASSES = ("gemm_input_proj", "gemm_dx", "gemm_dw", "gemm_dr", "gemm_dw_dr", "gemm_dp")
 
 
+def recurrence_model_bytes(wl, cls: str, launches_per_step: float):
+    """Algorithmic HBM bytes of one launch of a per-layer recurrence, in the
+    byte model of the training step: per step and batch row the forward reads
+    Gx_t and writes the activated gates (4H values each, fp32), c_t (fp32)
+    and h_t (bf16); the backward reads the gates and c_t (fp32) and dy_t
+    (bf16) and writes dz_t (4H, bf16); the recurrent weights are read once
+    (bf16).  The kernels keep Gx and the gates in fp16 where the layer allows
+    it, so they move fewer bytes than this model counts for the same work
+    (their own count is the kernel class's `gbs`).  None where a launch is
+    not one plain-LSTM layer (the layer wavefront, LSTMP layers)."""
+    if cls not in ("recurrent_fwd", "recurrent_bwd"):
+        return None
+    dirs = sum(2 if L.bidirectional else 1 for L in wl.layers)
+    if any(L.Hp for L in wl.layers) or abs(launches_per_step - dirs) > 1e-9:
+        return None
+    Hs = {L.H for L in wl.layers}
+    if len(Hs) != 1:
+        return None
+    H = Hs.pop()
+    per_row = (4 * H * 4 + 4 * H * 4 + H * 4 + H * 2) if cls == "recurrent_fwd" else \
+              (4 * H * 4 + H * 4 + H * 2 + 4 * H * 2)
+    return float(wl.T) * wl.B * per_row + 4.0 * H * H * 2
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1907_13257_amd", "csrc")
@@ -336,9 +360,12 @@ def main():
             roofline = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
                         "frac": ach / peak, "traffic": traffic}
         else:
-            ach = s["bytes"] / s["launches"] / avg_s / 1e9
+            kernel_bytes = s["bytes"] / s["launches"]
+            alg_bytes = recurrence_model_bytes(wl, dom, s["launches"] / args.steps) or kernel_bytes
+            ach = alg_bytes / avg_s / 1e9
             roofline = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic,
+                        "bytes_per_launch": alg_bytes, "kernel_bytes_per_launch": kernel_bytes}
             if dom.startswith("recurrent"):
                 # HBM is the only roofline that applies to the recurrences, but
                 # their counters (matrix cores and LDS a fraction busy, traffic
